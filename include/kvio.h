@@ -1,0 +1,190 @@
+/*
+ * kvio.h -- C ABI of libkvio.so: paged-KV transfers between pinned host memory
+ * and a GPU's paged KV pool, on AMD Instinct MI355X (gfx950).
+ *
+ * The operation is Strata's GPU-assisted I/O (Sec. 4.2, "Efficient KV Cache
+ * I/O"): instead of one DMA copy per small page, one kernel launch whose
+ * wavefronts each read a small chunk of the source into registers and stream
+ * it to the destination.  The source may be pinned host memory that the GPU
+ * reads directly over the host link.  Because every work item computes its
+ * own addresses, the kernel converts layouts on the fly (Sec. 4.2.1, Fig. 6):
+ * the host keeps one contiguous, transfer-friendly chunk per cached context,
+ * while the GPU keeps the compute-friendly, layer-first paged pool of Sec. 2.2.
+ *
+ * Layouts (R = num_kv_heads * head_dim * elem_bytes = bytes of one token row,
+ * P = page_size tokens, S = num_slots token slots per per-layer pool):
+ *   pool  : per layer l, one K array and one V array of S rows of R bytes,
+ *           token-major ([S][H][D]); slot s belongs to pool page s / P.
+ *   host  : one chunk per cached context, layer-major then K before V, then
+ *           token-major: row (l, kv, t) starts at byte
+ *           ((l * 2 + kv) * host_tokens + t) * R of the chunk (kv 0 = K, 1 = V).
+ *   pages : page_idx[j] is the pool page that holds context page j, so token
+ *           t lives in slot page_idx[t / P] * P + t % P.  At P = 1 the page
+ *           table is the slot list.
+ *
+ * Semantics of a transfer of context tokens [0, num_tokens) over the layer
+ * range [layer_begin, layer_end):
+ *   load    : pool row slot(t) of layer l, K or V  := host row (l, kv, t)
+ *   offload : host row (l, kv, t) := pool row slot(t)
+ * No other pool byte (load) or host byte (offload) is written.  The tail of a
+ * partial last page is left untouched.
+ *
+ * Conventions
+ *   - Every call returns kvio_status (0 = OK, negative = error); no exception
+ *     crosses the ABI.  On error kvio_last_error() holds a thread-local text.
+ *   - Transfers are asynchronous on the given stream (NULL = the default
+ *     stream); completion follows stream order.  Validation errors are
+ *     reported synchronously and enqueue nothing.
+ *   - The caller owns every buffer: pools, host chunks, page tables.  The
+ *     library owns only the pool handle (a device copy of the layer-pointer
+ *     table and a device error record).
+ *   - A pool handle is immutable after creation and may be used from several
+ *     threads and streams at once.  Transfers that run concurrently must write
+ *     disjoint bytes; a load whose page tables name one pool slot twice leaves
+ *     that slot holding one of the rows (unspecified which).
+ *   - Page indices are range-checked on the device at no measurable cost: a
+ *     row whose page lies outside [0, S / P) is skipped, never dereferenced,
+ *     and the first such (span, context page) is recorded for kvio_check().
+ */
+#ifndef KVIO_H
+#define KVIO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same opaque handle types as the HIP runtime API (redeclaring an identical
+ * typedef is legal in C11 and C++). */
+typedef struct ihipStream_t *hipStream_t;
+typedef struct ihipEvent_t *hipEvent_t;
+
+typedef enum kvio_status {
+    KVIO_OK = 0,
+    KVIO_EINVAL = -1,      /* null pointer, bad size, bad layer range, num_tokens > host_tokens,
+                              buffer smaller than the transfer reaches                        */
+    KVIO_ERANGE = -2,      /* kvio_check: a page index was outside [0, S / P)                */
+    KVIO_EALIGN = -3,      /* R, a pool layer or a host chunk not 16-byte aligned            */
+    KVIO_ENOTMAPPED = -4,  /* host chunk not accessible from the device (e.g. plain malloc)  */
+    KVIO_EHIP = -5,        /* a HIP runtime call failed; its message is in kvio_last_error  */
+    KVIO_ENOMEM = -6       /* allocation failed                                              */
+} kvio_status;
+
+/* Host chunk layouts.  Only the layer-major, token-major layout above exists. */
+#define KVIO_HOST_TOKEN_MAJOR 0
+
+/* Launch shaping (Sec. 4.2: a small number of large workgroups keeps the I/O
+ * kernel on few compute units; cache bypass limits pollution).  Zero fields
+ * take the library defaults.  Results never depend on these. */
+#define KVIO_LAUNCH_CACHED 0x1     /* plain loads/stores instead of non-temporal ones */
+typedef struct kvio_launch {
+    int32_t workgroups;   /* workgroups per launch, >= 1; 0 = default                       */
+    int32_t threads;      /* threads per workgroup: multiple of 64 in [64, 1024]; 0 = default */
+    int32_t tile_kib;     /* bytes each wavefront moves per step, in KiB: 4, 8 or 16; 0 = default */
+    int32_t flags;        /* KVIO_LAUNCH_* bits                                              */
+} kvio_launch;
+
+/* Describes caller-owned device memory; copied by kvio_pool_create. */
+typedef struct kvio_pool_desc {
+    int32_t num_layers;       /* L >= 1                                                  */
+    int32_t num_kv_heads;     /* H >= 1                                                  */
+    int32_t head_dim;         /* D >= 1                                                  */
+    int32_t elem_bytes;       /* bytes per element (2 for fp16/bf16); R % 16 must be 0  */
+    int32_t page_size;        /* P >= 1 tokens                                           */
+    int32_t host_layout;      /* KVIO_HOST_TOKEN_MAJOR                                   */
+    int64_t num_slots;        /* S token slots per per-layer pool, S % P == 0, S < 2^31 */
+    void *const *k_layers;    /* host array of L device pointers, each S * R bytes       */
+    void *const *v_layers;    /* host array of L device pointers, each S * R bytes       */
+    kvio_launch load_launch;  /* launch shape of load kernels                            */
+    kvio_launch offload_launch; /* launch shape of offload kernels                       */
+} kvio_pool_desc;
+
+typedef struct kvio_pool *kvio_pool_t;
+
+/* One cached context (one "span" of a batched transfer). */
+typedef struct kvio_span {
+    void *host;               /* pinned, device-mapped host chunk (or device memory),
+                                 16-byte aligned, >= L * 2 * host_tokens * R bytes     */
+    int64_t host_tokens;      /* token capacity of the chunk: its per-(layer, K|V) stride */
+    int64_t num_tokens;       /* move context tokens [0, num_tokens); <= host_tokens     */
+    const int32_t *page_idx;  /* DEVICE int32[ceil(num_tokens / P)]                      */
+} kvio_span;
+
+/* Most spans one kernel launch carries; a larger batch is split into
+ * consecutive launches on the same stream. */
+#define KVIO_MAX_SPANS_PER_LAUNCH 64
+
+/* Create a pool handle on the current device.  Checks that every layer
+ * pointer is device memory of at least S * R bytes and 16-byte aligned
+ * (KVIO_EINVAL / KVIO_EALIGN), then allocates the handle (KVIO_ENOMEM /
+ * KVIO_EHIP).  *out is set only on success. */
+kvio_status kvio_pool_create(const kvio_pool_desc *desc, kvio_pool_t *out);
+
+/* Free the handle.  The caller must have synchronised every stream that still
+ * runs a transfer on it.  NULL is accepted. */
+kvio_status kvio_pool_destroy(kvio_pool_t pool);
+
+/* Load (Sec. 4.2): move tokens [0, num_tokens) of each of the n_spans contexts,
+ * layers [layer_begin, layer_end), from the host chunks into the pool, in one
+ * launch per KVIO_MAX_SPANS_PER_LAUNCH spans.  Host reads are sequential per
+ * (layer, K|V); pool writes are scattered by page.  n_spans == 0 or all
+ * num_tokens == 0 enqueues nothing and returns KVIO_OK. */
+kvio_status kvio_load(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
+                      int32_t layer_begin, int32_t layer_end, hipStream_t stream);
+
+/* Offload (Sec. 4.1 backup to lower tiers; Sec. 4.2 I/O kernel): the inverse
+ * gather, pool rows into the contiguous host chunks.  Host bytes of rows
+ * t >= num_tokens are not written.  Duplicate page indices are allowed. */
+kvio_status kvio_offload(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
+                         int32_t layer_begin, int32_t layer_end, hipStream_t stream);
+
+/* Layer-wise load (Sec. 4.1: the executor waits until a layer's KV cache is
+ * present before computing that layer; Sec. 3.2 / Sec. 4.2.1 layer-wise
+ * overlap): kvio_load of the single layer `layer` on `stream`, then, if `done`
+ * is not NULL, hipEventRecord(done, stream), also when there was nothing to
+ * move.  A compute stream that waits on `done` may use layer `layer`. */
+kvio_status kvio_load_layer(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
+                            int32_t layer, hipStream_t stream, hipEvent_t done);
+
+/* Synchronise the device, then report and clear the device error record:
+ * KVIO_ERANGE (with the span and context page in kvio_last_error) if an
+ * earlier transfer met an out-of-range page index, else KVIO_OK. */
+kvio_status kvio_check(kvio_pool_t pool);
+
+/* Naive baseline (Sec. 3.1, the DMA path of the baselines): one
+ * hipMemcpyAsync per contiguous (page, layer, K|V) segment of up to P rows,
+ * all on `stream`.  Same arguments and result as kvio_load / kvio_offload.
+ * Page indices are validated on the host first (KVIO_ERANGE), so the
+ * page tables must be readable from the host here: host memory or pinned
+ * memory, or device memory (copied to the host first, synchronously). */
+kvio_status kvio_naive_load(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
+                            int32_t layer_begin, int32_t layer_end, hipStream_t stream);
+kvio_status kvio_naive_offload(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
+                               int32_t layer_begin, int32_t layer_end, hipStream_t stream);
+
+/* One contiguous hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, stream):
+ * the host-link peak that the transfers are measured against. */
+kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);
+
+/* Pinned, device-mapped host memory for host chunks (hipHostMalloc).
+ * flags: KVIO_HOST_COHERENT (fine-grained, the default) or
+ * KVIO_HOST_NONCOHERENT (coarse-grained).  The returned pointer is also the
+ * device address.  Free with kvio_host_free. */
+#define KVIO_HOST_COHERENT 0x0
+#define KVIO_HOST_NONCOHERENT 0x1
+kvio_status kvio_host_alloc(size_t bytes, uint32_t flags, void **out);
+kvio_status kvio_host_free(void *ptr);
+
+/* Static text for a status code. */
+const char *kvio_strerror(kvio_status status);
+
+/* Thread-local detail of the last failure on this thread ("" if none). */
+const char *kvio_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVIO_H */
