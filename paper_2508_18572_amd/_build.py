@@ -1,0 +1,35 @@
+"""Build libkvio.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree."""
+import os
+import subprocess
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG, "libkvio.so")
+SOURCES = [os.path.join(CSRC, "kvio_kernels.hip"), os.path.join(CSRC, "kvio_api.cpp")]
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+FLAGS = [
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "-Wall", "-Wextra", "-Werror", "-Wno-unused-parameter",
+    # keep the compiler from forming packed fp32 ops (there are no fp32 ops
+    # here, but every HIP source of this project is built this way)
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", INCLUDE, "-I", CSRC,
+]
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    """Compile every source into libkvio.so; always recompiles."""
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC] + FLAGS + list(extra) + SOURCES + ["-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

