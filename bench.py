@@ -59,9 +59,35 @@ def parse():
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-peak", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0,
+                    help="only run a plain device-to-device elementwise copy of this many bytes, three "
+                         "times (the known-size kernel that scales the HBM byte counters), then exit")
     ap.add_argument("--naive-tokens", type=int, default=2048,
                     help="tokens of the context the naive per-page baseline copies (all layers)")
     return ap.parse_args()
+
+
+def measured_traffic(config, default_launch):
+    """HBM/link bytes per load launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel sources (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "kvio_copy_kernel__llama8b_p1_32k.counters.txt")
+    if config != 2 or not default_launch or not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            key, val = line.split(":", 1)
+            kv[key.strip()] = val.strip()
+    csrc = os.path.join(ROOT, "paper_2508_18572_amd", "csrc")
+    cur = " ".join(hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest()
+                   for f in ("kvio_kernels.hip", "kvio_internal.h"))
+    if cur != kv.get("kernel_sources_sha256"):
+        return None
+    fetch = float(kv["load_fetch_kib"]) * float(kv["fetch_scale"]) * 1024
+    write = float(kv["load_write_kib"]) * float(kv["write_scale"]) * 1024
+    return {"bytes": round(fetch + write), "fetch_bytes": round(fetch), "write_bytes": round(write),
+            "source": os.path.relpath(path, ROOT)}
 
 
 def log(msg):
@@ -157,6 +183,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy
+        src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.bitwise_not(src, out=dst)      # reads n bytes, writes n bytes
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes_read": n, "calibration_copy_bytes_written": n,
+                          "launches": 3}), flush=True)
+        return
     k = args.config
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -267,6 +303,8 @@ def main():
                          f"({len(os.sched_getaffinity(0))} cores available, 1 used)"}
         log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
 
+    default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host)
+    traffic = measured_traffic(k, default_launch)
     frac_h2d = load_gbps / peak["h2d"] if peak else None
     frac_d2h = off_gbps / peak["d2h"] if peak else None
     ideal_ms = (payload / (peak["h2d"] * GB) + payload / (peak["d2h"] * GB)) * 1e3 if peak else None
@@ -300,8 +338,11 @@ def main():
         "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
         "roofline": {"bound": "host_link", "kernel": "kvio_copy_kernel<load>",
                      "achieved": round(load_gbps, 3), "peak": round(peak["h2d"], 3) if peak else None,
-                     "unit": "GB/s", "frac": round(frac_h2d, 4) if peak else None, "traffic": None,
+                     "unit": "GB/s", "frac": round(frac_h2d, 4) if peak else None,
+                     "traffic": traffic["bytes"] if traffic else None,
+                     "traffic_detail": traffic,
                      "algorithmic_bytes_per_launch": payload,
+                     "algorithmic_traffic_per_launch": 2 * payload,
                      "pcie_spec_peak": PCIE_SPEC_GBPS, "frac_of_spec": round(load_gbps / PCIE_SPEC_GBPS, 4),
                      "hbm": {"achieved": round(load_gbps, 3), "peak": HBM_PEAK_GBPS,
                              "frac": round(load_gbps / HBM_PEAK_GBPS, 5)}},
