@@ -1,0 +1,230 @@
+"""The five evaluation workloads at full size, through the C ABI, in the launch
+configuration bench.py times (library defaults), checked against the CPU
+oracle on sampled rows and by properties that hold at any size:
+
+  * sampled rows: the oracle's slot for (span, layer, kv, token) holds exactly
+    the host row at the oracle's host offset;
+  * untouched slots keep their sentinel and every touched slot changed
+    (plain torch comparisons over the whole pool);
+  * round trip: offloading the loaded context into a fresh chunk reproduces
+    the source chunk byte for byte.
+
+Inputs are seeded (workloads module): data seed k, placement seed 100 + k,
+churn seed 200 + k for workload k.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from _kvtest import SENTINEL, memequal, sampled_rows_match, touched_mask, untouched_rows_hold_sentinel
+
+pytestmark = pytest.mark.gpu
+
+GiB = 1 << 30
+
+
+@pytest.fixture(scope="module")
+def kv():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an AMD GPU"
+    import paper_2508_18572_amd as kv
+    return kv
+
+
+def new_pool(L, S, H, D, dtype):
+    import torch
+    pool = torch.empty((2, L, S, H, D), dtype=dtype, device="cuda")
+    pool.view(torch.int16).fill_(SENTINEL)
+    return pool
+
+
+def test_workload1_tiny_pool_exact(kv):
+    """Tiny pool: the whole pool image and the round trip are compared byte for byte."""
+    import torch
+    wl = W.WORKLOADS[1]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    pages = W.random_pages(np.random.default_rng(W.placement_seed(1)), S // P, T // P)
+    pool_t = new_pool(L, S, H, D, torch.float16)
+    pool_np = pool_t.cpu().numpy().view(np.uint8).reshape(2, L, S, R).copy()
+    with kv.HostBuffer(L * 2 * T * R) as hb, kv.HostBuffer(L * 2 * T * R) as ob:
+        W.fill_np(hb.array, W.data_seed(1), shp)
+        pt = torch.from_numpy(pages).cuda()
+        pool = kv.KVPool(pool_t, P)
+        pool.load([(hb.ptr, T, T, pt.data_ptr())])
+        ob.array[:] = 0
+        pool.offload([(ob.ptr, T, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, [(hb.array, T, T, pages)])
+        assert np.array_equal(pool_t.cpu().numpy().view(np.uint8).reshape(2, L, S, R), exp)
+        assert np.array_equal(ob.array, hb.array)
+        # 1000 back-to-back loads leave the same image (steady-state path)
+        for _ in range(1000):
+            pool.load([(hb.ptr, T, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        assert np.array_equal(pool_t.cpu().numpy().view(np.uint8).reshape(2, L, S, R), exp)
+        pool.close()
+
+
+def single_context_workload(kv, k, layerwise=False):
+    import torch
+    wl = W.WORKLOADS[k]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    nbytes = L * 2 * T * R
+    rng = np.random.default_rng(W.placement_seed(k))
+    pages = W.random_slots(rng, S, T) if P == 1 else W.random_pages(rng, S // P, -(-T // P))
+    pool_t = new_pool(L, S, H, D, torch.bfloat16)
+    pt = torch.from_numpy(pages).cuda()
+    with kv.HostBuffer(nbytes) as hb, kv.HostBuffer(nbytes) as ob:
+        W.fill_cuda(hb.ptr, nbytes, W.data_seed(k), shp)
+        pool = kv.KVPool(pool_t, P)
+        span = [(hb.ptr, T, T, pt.data_ptr())]
+        if layerwise:
+            side = torch.cuda.Stream()
+            compute = torch.cuda.current_stream()
+            for l in range(L):
+                ev = torch.cuda.Event()
+                ev.record(side)
+                pool.load_layer(span, l, stream=side, done=ev)
+                compute.wait_event(ev)
+                pool_t[:, l, :1].float().sum()   # a compute-stream consumer of layer l
+        else:
+            pool.load(span)
+        torch.cuda.synchronize()
+        pool.check()
+        spans_np = [(hb.array, T, T, pages)]
+        assert sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k) == 4096
+        untouched_rows_hold_sentinel(pool_t, touched_mask(spans_np, P, S), L)
+        pool.offload([(ob.ptr, T, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        pool.check()
+        assert memequal(ob.ptr, hb.ptr, nbytes), "offload round trip differs from the host chunk"
+        pool.close()
+
+
+def test_workload2_llama8b_page1(kv):
+    single_context_workload(kv, 2)
+
+
+def test_workload3_70b_layerwise(kv):
+    single_context_workload(kv, 3, layerwise=True)
+
+
+def test_workload4_batched_churned(kv):
+    """64 partial-hit contexts of the 8B shape at page size 16 into a churned pool,
+    one batched kvio_load per wave (one wave when host memory allows)."""
+    import torch
+    k = 4
+    shp = W.LLAMA8B
+    L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
+    R = shp.row_bytes
+    req = W.batched_requests(k)
+    S = req.pool_pages * P
+    hit = [int(h) for h in req.hit_tokens]
+    sizes = [L * 2 * h * R for h in hit]
+    # Pinned host memory on the test box is capped (64 GiB per process), so the
+    # contexts are loaded in waves of at most 40 GiB of host chunks, each wave
+    # one batched kvio_load; the pool holds all of them.
+    budget = 40 * GiB
+    waves, cur, acc = [], [], 0
+    for i, b in enumerate(sizes):
+        if cur and acc + b > budget:
+            waves.append(cur)
+            cur, acc = [], 0
+        cur.append(i)
+        acc += b
+    waves.append(cur)
+    print(f"[workload4] {sum(hit)} tokens, {sum(sizes) / GiB:.1f} GiB, pool {S} slots, "
+          f"{len(waves)} wave(s), mean run length {req.mean_run_length:.2f}", flush=True)
+    pool_t = new_pool(L, S, H, D, torch.bfloat16)
+    pool = kv.KVPool(pool_t, P)
+    pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
+    all_spans_np = []
+    for w in waves:
+        nb = sum(sizes[i] for i in w)
+        with kv.HostBuffer(nb) as hb:
+            offs, o = {}, 0
+            for i in w:
+                offs[i] = o
+                W.fill_cuda(hb.ptr + o, sizes[i], W.data_seed(k) * 1000 + i, shp)
+                o += sizes[i]
+            spans = [(hb.ptr + offs[i], hit[i], hit[i], pts[i].data_ptr()) for i in w]
+            pool.load(spans)
+            torch.cuda.synchronize()
+            pool.check()
+            spans_np = [(hb.array[offs[i]:offs[i] + sizes[i]], hit[i], hit[i], req.page_lists[i]) for i in w]
+            sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k + len(all_spans_np))
+            # round trip of every span through one scratch chunk
+            big = max(sizes[i] for i in w)
+            with kv.HostBuffer(big) as sb:
+                for i in w:
+                    pool.offload([(sb.ptr, hit[i], hit[i], pts[i].data_ptr())])
+                    torch.cuda.synchronize()
+                    assert memequal(sb.ptr, hb.ptr + offs[i], sizes[i]), f"span {i} round trip differs"
+            pool.check()
+            all_spans_np += [(None, hit[i], hit[i], req.page_lists[i]) for i in w]
+    # churn-resident pages and every slot of no request keep the sentinel
+    untouched_rows_hold_sentinel(pool_t, touched_mask(all_spans_np, P, S), L)
+    pool.close()
+
+
+def test_workload5_1m_with_concurrent_offload(kv):
+    """1M-token load at page size 1 on one stream while 16K other slots are
+    offloaded repeatedly to a separate host chunk on a second stream."""
+    import torch
+    k = 5
+    wl = W.WORKLOADS[k]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    TO = 16384
+    rng = np.random.default_rng(W.placement_seed(k))
+    both = W.random_slots(rng, S, T + TO)
+    load_slots, off_slots = both[:T].copy(), both[T:].copy()
+    nb, nbo = L * 2 * T * R, L * 2 * TO * R
+    pool_t = new_pool(L, S, H, D, torch.bfloat16)
+    pool = kv.KVPool(pool_t, P)
+    pl, po = torch.from_numpy(load_slots).cuda(), torch.from_numpy(off_slots).cuda()
+    with kv.HostBuffer(nb) as hb, kv.HostBuffer(nbo) as src_o, kv.HostBuffer(nbo) as dst_o:
+        W.fill_cuda(hb.ptr, nb, W.data_seed(k), shp)
+        W.fill_cuda(src_o.ptr, nbo, W.data_seed(k) * 1000 + 1, shp)
+        pool.load([(src_o.ptr, TO, TO, po.data_ptr())])          # set-up: resident data to offload
+        torch.cuda.synchronize()
+        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+        done = torch.cuda.Event()
+        pool.load([(hb.ptr, T, T, pl.data_ptr())], stream=sa)
+        done.record(sa)
+        runs = 0
+        while True:
+            pool.offload([(dst_o.ptr, TO, TO, po.data_ptr())], stream=sb)
+            runs += 1
+            sb.synchronize()
+            if done.query() or runs >= 200:
+                break
+        torch.cuda.synchronize()
+        pool.check()
+        print(f"[workload5] {runs} concurrent offload runs during the 1M-token load", flush=True)
+        assert memequal(dst_o.ptr, src_o.ptr, nbo), "concurrent offload differs from its source"
+        spans_np = [(hb.array, T, T, load_slots), (src_o.array, TO, TO, off_slots)]
+        sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k)
+        untouched_rows_hold_sentinel(pool_t, touched_mask(spans_np, P, S), L)
+        # Round trip in token ranges through a 4 GiB chunk (pinned memory is
+        # capped at 64 GiB per process on the test box): offloading tokens
+        # [a, b) uses the page table from entry a and a chunk of b - a tokens.
+        piece = (4 * GiB) // (L * 2 * R)
+        with kv.HostBuffer(L * 2 * piece * R) as ob:
+            for a in range(0, T, piece):
+                n = min(piece, T - a)
+                pool.offload([(ob.ptr, n, n, pl.data_ptr() + 4 * a)])
+                torch.cuda.synchronize()
+                for plane in range(2 * L):
+                    assert memequal(ob.ptr + plane * n * R, hb.ptr + (plane * T + a) * R, n * R), \
+                        f"1M-token round trip differs in tokens [{a}, {a + n}) plane {plane}"
+    pool.check()
+    pool.close()
