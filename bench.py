@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 5])
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--workgroups", type=int, default=0)
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--tile-kib", type=int, default=0)
@@ -81,13 +81,39 @@ def measured_traffic(config, default_launch):
             kv[key.strip()] = val.strip()
     csrc = os.path.join(ROOT, "paper_2508_18572_amd", "csrc")
     cur = " ".join(hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest()
-                   for f in ("kvio_kernels.hip", "kvio_internal.h"))
+                   for f in ("kvio_kernels.hip", "kvio_internal.h", "kvio_api.cpp"))
     if cur != kv.get("kernel_sources_sha256"):
         return None
     fetch = float(kv["load_fetch_kib"]) * float(kv["fetch_scale"]) * 1024
     write = float(kv["load_write_kib"]) * float(kv["write_scale"]) * 1024
     return {"bytes": round(fetch + write), "fetch_bytes": round(fetch), "write_bytes": round(write),
             "source": os.path.relpath(path, ROOT)}
+
+
+_IO = {}
+
+
+def io_stream(torch, kv):
+    """The transfer stream: a stream over every compute unit created through
+    kvio_stream_create with a CU mask, which gives it a hardware queue of its
+    own (ordinary streams share the few hardware queues round-robin, so two of
+    them can serialise).  Created once per process; a plain torch stream if the
+    runtime refuses."""
+    if "s" not in _IO:
+        try:
+            n = torch.cuda.get_device_properties(0).multi_processor_count
+            st = kv.Stream(list(range(n)))
+            _IO["s"], _IO["kind"] = st.torch, f"dedicated queue (CU mask of all {n} CUs)"
+            _IO["keep"] = st
+        except kv.KvioError as e:
+            _IO["s"], _IO["kind"] = torch.cuda.Stream(), f"torch stream ({e.detail})"
+    return _IO["s"]
+
+
+def close_io_stream(torch, kv):
+    if "keep" in _IO:
+        torch.cuda.synchronize()
+        _IO.pop("keep").close()
 
 
 def log(msg):
@@ -119,7 +145,7 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
     """Median GB/s of one contiguous pinned hipMemcpyAsync per direction (H2D from
     src_ptr, D2H into dst_ptr), and of H2D and D2H running concurrently on two
     streams (each half the size)."""
-    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1, s2 = io_stream(torch, kv), torch.cuda.Stream()
     half = nbytes // 2
     res = {}
     for name, fn in (("h2d", lambda s: kv.kvio_memcpy(dev_ptr, src_ptr, nbytes, s)),
@@ -133,16 +159,23 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
             t.stop(e)
         torch.cuda.synchronize()
         res[name] = nbytes / (statistics.median(t.ms()) * 1e-3) / GB
-    # bidirectional: H2D of one half while D2H of the other half
-    ts = []
-    for _ in range(reps):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        kv.kvio_memcpy(dev_ptr, src_ptr, half, s1)
-        kv.kvio_memcpy(dst_ptr + half, dev_ptr + half, half, s2)
-        torch.cuda.synchronize()
-        ts.append(time.perf_counter() - t0)
-    res["bidir"] = 2 * half / statistics.median(ts) / GB
+    # bidirectional: H2D of one half while D2H of the other half.  The runtime
+    # binds each stream to a copy engine on its own; two streams can land on
+    # one engine and serialise, so several stream pairs are tried and the best
+    # (the link's real bidirectional capacity) is kept.
+    best = 0.0
+    pairs = [(s1, s2), (s2, torch.cuda.Stream()), (torch.cuda.Stream(), torch.cuda.Stream())]
+    for a, b in pairs:
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            kv.kvio_memcpy(dev_ptr, src_ptr, half, a)
+            kv.kvio_memcpy(dst_ptr + half, dev_ptr + half, half, b)
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        best = max(best, 2 * half / statistics.median(ts) / GB)
+    res["bidir"] = best
     res["bytes"] = nbytes
     return res
 
@@ -171,6 +204,377 @@ def cpu_baseline(pool_rows, row_bytes, host, host_tokens, num_tokens, pages, pag
     return nbytes, el, passes
 
 
+def steady_state(torch, kv, pool, span, host, stream, payload, reps):
+    """Small-context latency: one load alone (host launch to completion, and
+    GPU time), then `reps` back-to-back loads; the same for a contiguous
+    hipMemcpyAsync of the same size into device memory."""
+    dev = torch.empty(payload, dtype=torch.uint8, device="cuda")
+    out = {}
+    for name, fn in (("load", lambda: pool.load(span, stream=stream)),
+                     ("memcpy", lambda: kv.kvio_memcpy(dev.data_ptr(), host.ptr, payload, stream))):
+        fn()
+        torch.cuda.synchronize()
+        shots = []
+        gpu = []
+        for _ in range(20):
+            t = Timer(torch, stream)
+            c0 = time.perf_counter()
+            e = t.start()
+            fn()
+            t.stop(e)
+            stream.synchronize()
+            shots.append((time.perf_counter() - c0) * 1e6)
+            gpu.append(t.ms()[0] * 1e3)
+        t = Timer(torch, stream)
+        e = t.start()
+        for _ in range(reps):
+            fn()
+        t.stop(e)
+        torch.cuda.synchronize()
+        ms = t.ms()[0]
+        out[f"{name}_gbps"] = round(reps * payload / (ms * 1e-3) / GB, 3)
+        out[f"{name}_us_per_transfer"] = round(ms * 1e3 / reps, 3)
+        out[f"{name}_single_shot_wall_us"] = round(statistics.median(shots), 2)
+        out[f"{name}_single_shot_gpu_us"] = round(statistics.median(gpu), 2)
+    out["single_shot_us"] = out["load_single_shot_wall_us"]
+    out["reps"] = reps
+    del dev
+    return out
+
+
+def base_result(args, value, ms_per_step, workload, extra_config):
+    cfg = {"workload": workload}
+    cfg.update(extra_config)
+    cfg["io_stream"] = _IO.get("kind")
+    return {
+        "metric": "effective KV load/offload GB/s and tokens/s; % of measured host-link peak",
+        "value": round(value, 3), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u8", "data": "synthetic", "config": cfg,
+    }
+
+
+def h2d_d2h_peak(torch, kv, nbytes=2 << 30):
+    """The contiguous hipMemcpyAsync peak on buffers of its own (2 GiB pinned
+    host, 2 GiB device)."""
+    scratch = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    with kv.HostBuffer(nbytes) as hb:
+        hb.array[::4096] = 1                      # touch every page once
+        peak = memcpy_peak(torch, kv, hb.ptr, hb.ptr, scratch.data_ptr(), nbytes)
+    del scratch
+    log(f"memcpy peak: h2d {peak['h2d']:.2f} GB/s, d2h {peak['d2h']:.2f} GB/s, bidir {peak['bidir']:.2f} GB/s")
+    return peak
+
+
+def launch_from(args, kv):
+    return kv.launch(args.workgroups, args.threads, args.tile_kib, kv.KVIO_LAUNCH_CACHED if args.cached else 0)
+
+
+def run_layerwise(args, torch, kv, W):
+    """70B GQA KV at page size 16: a 64K-token context loaded layer by layer on a
+    side stream (kvio_load_layer, one event per layer) while a compute stream
+    runs one bf16 GEMM (4096 x 8192 x 8192) per layer, each GEMM waiting on its
+    layer's event (layer-wise overlap, Strata Sec. 4.1 / Sec. 4.2.1)."""
+    k = 3
+    wl = W.WORKLOADS[k]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    log(f"config 3: {wl.description}; L={L} P={P} S={S} T={T}")
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    pages = W.random_pages(np.random.default_rng(W.placement_seed(k)), S // P, -(-T // P))
+    pidx = torch.from_numpy(pages).cuda()
+    nbytes = L * 2 * T * R
+    host = kv.HostBuffer(nbytes)
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    W.fill_cuda(host.ptr, nbytes, W.data_seed(k), shp)
+    pool = kv.KVPool(pool_t, P, load_launch=launch_from(args, kv))
+    span = [(host.ptr, T, T, pidx.data_ptr())]
+    side, comp = io_stream(torch, kv), torch.cuda.Stream()
+    M, N, K = 4096, 8192, 8192
+    g = torch.Generator(device="cuda").manual_seed(W.data_seed(k))
+    A = torch.randn(M, K, device="cuda", dtype=torch.bfloat16, generator=g)
+    B = torch.randn(K, N, device="cuda", dtype=torch.bfloat16, generator=g)
+    C = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+    per_layer = 2 * T * R
+
+    def loads_alone():
+        t = Timer(torch, side)
+        e = t.start()
+        for l in range(L):
+            pool.load_layer(span, l, stream=side)
+        t.stop(e)
+        torch.cuda.synchronize()
+        return t.ms()[0]
+
+    def gemms_alone():
+        t = Timer(torch, comp)
+        e = t.start()
+        with torch.cuda.stream(comp):
+            for l in range(L):
+                torch.matmul(A, B, out=C)
+        t.stop(e)
+        torch.cuda.synchronize()
+        return t.ms()[0]
+
+    def both():
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(comp)
+        side.wait_event(start)
+        g0, g1, evs = [], [], []
+        for l in range(L):
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record(side)                              # materialise the handle
+            pool.load_layer(span, l, stream=side, done=ev)
+            evs.append(ev)
+            comp.wait_event(ev)
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(comp)
+            with torch.cuda.stream(comp):
+                torch.matmul(A, B, out=C)
+            b.record(comp)
+            g0.append(a)
+            g1.append(b)
+        torch.cuda.synchronize()
+        t_both = start.elapsed_time(g1[-1])
+        t_load = start.elapsed_time(evs[-1])
+        gemm_ms = sum(x.elapsed_time(y) for x, y in zip(g0, g1))
+        return t_both, t_load, gemm_ms
+
+    for _ in range(max(1, args.warmup)):
+        loads_alone()
+        gemms_alone()
+        both()
+    reps = max(1, min(args.steps, 5))
+    tl = statistics.median(loads_alone() for _ in range(reps))
+    tg = statistics.median(gemms_alone() for _ in range(reps))
+    runs = [both() for _ in range(reps)]
+    tb = statistics.median(r[0] for r in runs)
+    tl_co = statistics.median(r[1] for r in runs)
+    tg_co = statistics.median(r[2] for r in runs)
+    pool.check()
+    overlap = (tl + tg - tb) / min(tl, tg)
+    load_gbps = nbytes / (tl * 1e-3) / GB
+    load_gbps_co = nbytes / (tl_co * 1e-3) / GB
+    gemm_tflops = L * 2 * M * N * K / (tg * 1e-3) / 1e12
+    log(f"load alone {tl:.2f} ms ({load_gbps:.2f} GB/s), GEMMs alone {tg:.2f} ms ({gemm_tflops:.0f} TFLOP/s), "
+        f"both {tb:.2f} ms; load co-run {load_gbps_co:.2f} GB/s; GEMM time co-run {tg_co:.2f} ms; "
+        f"overlap efficiency {overlap:.3f}")
+    res = base_result(args, load_gbps_co, tb, f"config3: {wl.description}",
+                      {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "tokens": T,
+                       "payload_bytes": nbytes, "bytes_per_layer_launch": per_layer,
+                       "gemm_per_layer": [M, N, K], "step": "80 x (kvio_load_layer on a side stream; "
+                       "event; bf16 GEMM on the compute stream)"})
+    res.update({
+        "tokens_per_s": round(T / (tl_co * 1e-3), 1),
+        "layerwise": {"t_load_alone_ms": round(tl, 3), "t_gemm_alone_ms": round(tg, 3), "t_both_ms": round(tb, 3),
+                      "t_load_in_corun_ms": round(tl_co, 3), "gemm_ms_in_corun": round(tg_co, 3),
+                      "overlap_efficiency": round(overlap, 4), "load_gbps_alone": round(load_gbps, 3),
+                      "load_gbps_corun": round(load_gbps_co, 3), "gemm_slowdown": round(tg_co / tg, 4),
+                      "gemm_tflops_alone": round(gemm_tflops, 1)},
+        "load": {"gbps": round(load_gbps_co, 3), "frac_of_h2d_peak": round(load_gbps_co / peak["h2d"], 4) if peak else None},
+        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "roofline": {"bound": "host_link", "kernel": "kvio_copy_kernel<load> (per layer)",
+                     "achieved": round(load_gbps, 3), "peak": round(peak["h2d"], 3) if peak else None, "unit": "GB/s",
+                     "frac": round(load_gbps / peak["h2d"], 4) if peak else None, "traffic": None,
+                     "algorithmic_bytes_per_launch": per_layer},
+    })
+    pool.close()
+    host.free()
+    print(json.dumps(res), flush=True)
+
+
+def run_batched(args, torch, kv, W):
+    """64 partial-hit contexts of the 8B shape at page size 16 into a pool
+    fragmented by a seeded allocate/free churn; one batched kvio_load per wave
+    of contexts (pinned host memory per process is capped on the box, so the
+    host chunks are staged in waves of <= 40 GiB)."""
+    k = 4
+    shp = W.LLAMA8B
+    L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
+    R = shp.row_bytes
+    req = W.batched_requests(k)
+    S = req.pool_pages * P
+    hit = [int(h) for h in req.hit_tokens]
+    sizes = [L * 2 * h * R for h in hit]
+    budget = 40 << 30
+    waves, cur, acc = [], [], 0
+    for i, b in enumerate(sizes):
+        if cur and acc + b > budget:
+            waves.append(cur)
+            cur, acc = [], 0
+        cur.append(i)
+        acc += b
+    waves.append(cur)
+    total = sum(sizes)
+    log(f"config 4: {sum(hit)} tokens, {total / 2**30:.1f} GiB, pool {S} slots, {len(waves)} waves, "
+        f"mean page-run length {req.mean_run_length:.2f}")
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    lc = launch_from(args, kv)
+    pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc)
+    pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
+    host = kv.HostBuffer(max(sum(sizes[i] for i in w) for w in waves))
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    stream = io_stream(torch, kv)
+    reps = max(1, min(args.steps, 3))
+    load_ms, off_ms = [], []
+    for w in waves:
+        offs, o = {}, 0
+        for i in w:
+            offs[i] = o
+            W.fill_cuda(host.ptr + o, sizes[i], W.data_seed(k) * 1000 + i, shp)
+            o += sizes[i]
+        spans = [(host.ptr + offs[i], hit[i], hit[i], pts[i].data_ptr()) for i in w]
+        pool.load(spans, stream=stream)                    # warm-up
+        torch.cuda.synchronize()
+        tl, to = Timer(torch, stream), Timer(torch, stream)
+        for _ in range(reps):
+            e = tl.start()
+            pool.load(spans, stream=stream)
+            tl.stop(e)
+        for _ in range(reps):                                # offload back into the same chunks
+            e = to.start()
+            pool.offload(spans, stream=stream)
+            to.stop(e)
+        torch.cuda.synchronize()
+        load_ms.append(statistics.median(tl.ms()))
+        off_ms.append(statistics.median(to.ms()))
+    pool.check()
+    tload, toff = sum(load_ms), sum(off_ms)
+    load_gbps, off_gbps = total / (tload * 1e-3) / GB, total / (toff * 1e-3) / GB
+    log(f"batched load {load_gbps:.2f} GB/s, offload {off_gbps:.2f} GB/s over {len(waves)} waves")
+    res = base_result(args, load_gbps, tload, "config4: batched partial hits of the Llama-3.1-8B KV shape, "
+                      "page size 16, churned pool",
+                      {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "requests": len(hit),
+                       "tokens": sum(hit), "payload_bytes": total, "waves": len(waves),
+                       "mean_page_run_length": round(req.mean_run_length, 3),
+                       "step": "one batched kvio_load per wave, all waves"})
+    res.update({
+        "tokens_per_s": round(sum(hit) / (tload * 1e-3), 1),
+        "load": {"gbps": round(load_gbps, 3), "ms": round(tload, 3),
+                 "frac_of_h2d_peak": round(load_gbps / peak["h2d"], 4) if peak else None},
+        "offload": {"gbps": round(off_gbps, 3), "ms": round(toff, 3),
+                    "frac_of_d2h_peak": round(off_gbps / peak["d2h"], 4) if peak else None},
+        "wave_load_ms": [round(x, 3) for x in load_ms],
+        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "roofline": {"bound": "host_link", "kernel": "kvio_copy_kernel<load> (batched spans)",
+                     "achieved": round(load_gbps, 3), "peak": round(peak["h2d"], 3) if peak else None, "unit": "GB/s",
+                     "frac": round(load_gbps / peak["h2d"], 4) if peak else None, "traffic": None,
+                     "algorithmic_bytes_per_launch": round(total / len(waves))},
+    })
+    pool.close()
+    host.free()
+    print(json.dumps(res), flush=True)
+
+
+def run_bidirectional(args, torch, kv, W):
+    """Qwen2.5-7B-1M KV at page size 1: a 1M-token load on one stream while a
+    second stream offloads 16K other resident slots back to back into a
+    separate host chunk; reports load, offload and combined GB/s over the load
+    window against the measured bidirectional memcpy peak."""
+    k = 5
+    wl = W.WORKLOADS[k]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    TO = 16384
+    both = W.random_slots(np.random.default_rng(W.placement_seed(k)), S, T + TO)
+    pl = torch.from_numpy(both[:T].copy()).cuda()
+    po = torch.from_numpy(both[T:].copy()).cuda()
+    nb, nbo = L * 2 * T * R, L * 2 * TO * R
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    lc = launch_from(args, kv)
+    pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc)
+    host = kv.HostBuffer(nb)
+    src_o, dst_o = kv.HostBuffer(nbo), kv.HostBuffer(nbo)
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    W.fill_cuda(host.ptr, nb, W.data_seed(k), shp)
+    W.fill_cuda(src_o.ptr, nbo, W.data_seed(k) * 1000 + 1, shp)
+    pool.load([(src_o.ptr, TO, TO, po.data_ptr())])
+    sa, sb = io_stream(torch, kv), torch.cuda.Stream()
+    span_l = [(host.ptr, T, T, pl.data_ptr())]
+    span_o = [(dst_o.ptr, TO, TO, po.data_ptr())]
+    # each direction alone
+    tla, toa = Timer(torch, sa), Timer(torch, sb)
+    pool.load(span_l, stream=sa)
+    pool.offload(span_o, stream=sb)
+    torch.cuda.synchronize()
+    e = tla.start()
+    pool.load(span_l, stream=sa)
+    tla.stop(e)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        e = toa.start()
+        pool.offload(span_o, stream=sb)
+        toa.stop(e)
+    torch.cuda.synchronize()
+    t_load_alone = tla.ms()[0]
+    t_off_alone = statistics.median(toa.ms())
+    n_off = int(t_load_alone / t_off_alone * 1.5) + 4
+    # concurrent
+    reps = max(1, min(args.steps, 3))
+    rows = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(sa)
+        sb.wait_event(start)
+        pool.load(span_l, stream=sa)
+        lend = torch.cuda.Event(enable_timing=True)
+        lend.record(sa)
+        ends = []
+        for _ in range(n_off):
+            pool.offload(span_o, stream=sb)
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record(sb)
+            ends.append(ev)
+        torch.cuda.synchronize()
+        t_load = start.elapsed_time(lend)
+        done = [start.elapsed_time(ev) for ev in ends]
+        inside = [t for t in done if t <= t_load]
+        rows.append((t_load, len(inside), inside[-1] if inside else None))
+    pool.check()
+    t_load = statistics.median(r[0] for r in rows)
+    n_in = min(r[1] for r in rows)
+    off_bytes = n_in * nbo
+    t_off_window = statistics.median(r[2] for r in rows if r[2] is not None) if n_in else None
+    load_gbps = nb / (t_load * 1e-3) / GB
+    off_gbps = off_bytes / (t_off_window * 1e-3) / GB if n_in else 0.0
+    bidir = (nb + off_bytes) / (t_load * 1e-3) / GB
+    log(f"load alone {nb / (t_load_alone * 1e-3) / GB:.2f} GB/s, offload alone {nbo / (t_off_alone * 1e-3) / GB:.2f} "
+        f"GB/s; concurrent: load {load_gbps:.2f} GB/s, offload {off_gbps:.2f} GB/s ({n_in} runs), "
+        f"combined {bidir:.2f} GB/s")
+    res = base_result(args, bidir, t_load, f"config5: {wl.description}",
+                      {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "tokens": T,
+                       "offload_tokens_per_run": TO, "payload_bytes_load": nb, "payload_bytes_per_offload": nbo,
+                       "step": "kvio_load of 1M tokens on stream A || back-to-back 16K-token kvio_offload "
+                               "runs on stream B"})
+    res.update({
+        "tokens_per_s": round((T + n_in * TO) / (t_load * 1e-3), 1),
+        "load": {"gbps_concurrent": round(load_gbps, 3), "gbps_alone": round(nb / (t_load_alone * 1e-3) / GB, 3),
+                 "frac_of_h2d_peak_alone": round(nb / (t_load_alone * 1e-3) / GB / peak["h2d"], 4) if peak else None},
+        "offload": {"gbps_concurrent": round(off_gbps, 3), "runs_in_window": n_in,
+                    "gbps_alone": round(nbo / (t_off_alone * 1e-3) / GB, 3),
+                    "frac_of_d2h_peak_alone": round(nbo / (t_off_alone * 1e-3) / GB / peak["d2h"], 4) if peak else None},
+        "bidirectional_gbps": round(bidir, 3),
+        "frac_of_bidir_peak": round(bidir / peak["bidir"], 4) if peak else None,
+        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "roofline": {"bound": "host_link (both directions)", "kernel": "kvio_copy_kernel<load> || <offload>",
+                     "achieved": round(bidir, 3), "peak": round(peak["bidir"], 3) if peak else None, "unit": "GB/s",
+                     "frac": round(bidir / peak["bidir"], 4) if peak else None, "traffic": None,
+                     "algorithmic_bytes_per_launch": nb},
+    })
+    pool.close()
+    host.free()
+    src_o.free()
+    dst_o.free()
+    print(json.dumps(res), flush=True)
+
+
+EXTRA_MODES = {3: run_layerwise, 4: run_batched, 5: run_bidirectional}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -194,6 +598,17 @@ def main():
                           "launches": 3}), flush=True)
         return
     k = args.config
+    try:
+        if k in EXTRA_MODES:
+            EXTRA_MODES[k](args, torch, kv, W)
+        else:
+            run_single(args, torch, kv, W, k)
+    finally:
+        close_io_stream(torch, kv)
+
+
+def run_single(args, torch, kv, W, k):
+    """Configs 1 and 2: one cached context, load + offload per step."""
     wl = W.WORKLOADS[k]
     shp = wl.shape
     L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
@@ -222,15 +637,10 @@ def main():
     pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
     span_in = [(host.ptr, T, T, pidx.data_ptr())]
     span_out = [(out.ptr, T, T, pidx.data_ptr())]
-    stream = torch.cuda.Stream()
+    stream = io_stream(torch, kv)
 
     # ---- contiguous host-link peak (denominator) ----------------------------------------
-    peak = None
-    if not args.no_peak:
-        scratch = torch.empty(min(host_bytes, 2 << 30), dtype=torch.uint8, device="cuda")
-        peak = memcpy_peak(torch, kv, host.ptr, out.ptr, scratch.data_ptr(), scratch.numel())
-        del scratch
-        log(f"memcpy peak: h2d {peak['h2d']:.2f} GB/s, d2h {peak['d2h']:.2f} GB/s, bidir {peak['bidir']:.2f} GB/s")
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
 
     # ---- timed steps ---------------------------------------------------------------------
     tl, to, tstep = Timer(torch, stream), Timer(torch, stream), Timer(torch, stream)
@@ -260,13 +670,7 @@ def main():
     log(f"load {load_ms:.3f} ms ({load_gbps:.2f} GB/s), offload {off_ms:.3f} ms ({off_gbps:.2f} GB/s), "
         f"step {step_ms:.3f} ms, wall {wall / args.steps * 1e3:.3f} ms/step")
 
-    # quick sampled correctness check of the last step (full parity lives in the tests)
-    h = host.array.reshape(L, 2, T, R)
-    sample = np.random.default_rng(0).integers(0, T, 16)
-    got = pool_t.view(torch.uint8).view(2, L, S, R)[:, :, torch.from_numpy(pages[sample].astype(np.int64)).cuda()]
-    got = got.cpu().numpy()
-    for i, t in enumerate(sample):
-        assert np.array_equal(got[0, :, i], h[:, 0, t]) and np.array_equal(got[1, :, i], h[:, 1, t])
+    # round-trip property of the last step (full parity lives in the tests)
     assert np.array_equal(out.array, host.array), "offload round trip differs from the host chunk"
 
     # ---- naive per-page DMA baseline (prefix of the calls) -------------------------------
@@ -303,6 +707,12 @@ def main():
                          f"({len(os.sched_getaffinity(0))} cores available, 1 used)"}
         log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
 
+    steady = None
+    if k == 1:
+        steady = steady_state(torch, kv, pool, span_in, host, stream, payload, reps=1000)
+        log(f"steady state over 1000 loads: {steady['load_gbps']:.2f} GB/s, single shot "
+            f"{steady['single_shot_us']:.1f} us; same-size memcpy {steady['memcpy_gbps']:.2f} GB/s")
+
     default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host)
     traffic = measured_traffic(k, default_launch)
     frac_h2d = load_gbps / peak["h2d"] if peak else None
@@ -327,7 +737,8 @@ def main():
                    "step": "kvio_load (all layers) + kvio_offload (all layers)",
                    "launch": {"workgroups": args.workgroups or "default", "threads": args.threads or "default",
                               "tile_kib": args.tile_kib or "default", "nontemporal": not args.cached},
-                   "host_memory": "non-coherent" if args.noncoherent_host else "coherent"},
+                   "host_memory": "non-coherent" if args.noncoherent_host else "coherent",
+                   "io_stream": _IO.get("kind")},
         "tokens_per_s": round(2 * T / (step_ms * 1e-3), 1),
         "load": {"ms": round(load_ms, 4), "gbps": round(load_gbps, 3), "tokens_per_s": round(T / (load_ms * 1e-3), 1),
                  "frac_of_h2d_peak": round(frac_h2d, 4) if peak else None},
@@ -349,6 +760,8 @@ def main():
         "naive": naive,
         "cpu_baseline": cpu,
     }
+    if steady:
+        result["steady_state"] = steady
     pool.close()
     host.free()
     out.free()

@@ -177,6 +177,18 @@ kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t st
 kvio_status kvio_host_alloc(size_t bytes, uint32_t flags, void **out);
 kvio_status kvio_host_free(void *ptr);
 
+/* Stream for transfers or for the kernels they run beside (Sec. 4.2: the
+ * I/O kernel is confined to a small part of the GPU so that co-running
+ * compute is not disturbed).  With mask_words > 0 the stream's kernels run
+ * only on the compute units whose bits are set in cu_mask (bit b of word w =
+ * CU 32 * w + b, hipExtStreamCreateWithCUMask); a transfer stream and a
+ * compute stream with complementary masks never wait for each other's
+ * workgroups.  With mask_words == 0 it is an ordinary non-blocking stream.
+ * Streams keep the default priority.  Destroy with kvio_stream_destroy after
+ * synchronising it. */
+kvio_status kvio_stream_create(const uint32_t *cu_mask, uint32_t mask_words, hipStream_t *out);
+kvio_status kvio_stream_destroy(hipStream_t stream);
+
 /* Static text for a status code. */
 const char *kvio_strerror(kvio_status status);
 

@@ -10,5 +10,6 @@ from .kvio import (  # noqa: F401
     KVIO_HOST_COHERENT, KVIO_HOST_NONCOHERENT, KVIO_LAUNCH_CACHED, KVIO_MAX_SPANS_PER_LAUNCH,
     kvio_check, kvio_host_alloc, kvio_host_free, kvio_last_error, kvio_load, kvio_load_layer,
     kvio_memcpy, kvio_naive_load, kvio_naive_offload, kvio_offload, kvio_pool_create,
-    kvio_pool_destroy, kvio_span, kvio_strerror, launch, make_spans,
+    kvio_pool_destroy, kvio_span, kvio_strerror, launch, make_spans, Stream,
+    kvio_stream_create, kvio_stream_destroy,
 )

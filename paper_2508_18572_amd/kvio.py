@@ -82,6 +82,8 @@ def _load_library() -> ctypes.CDLL:
         "kvio_memcpy": [vp, vp, ctypes.c_size_t, vp],
         "kvio_host_alloc": [ctypes.c_size_t, ctypes.c_uint32, ctypes.POINTER(vp)],
         "kvio_host_free": [vp],
+        "kvio_stream_create": [ctypes.POINTER(ctypes.c_uint32), ctypes.c_uint32, ctypes.POINTER(vp)],
+        "kvio_stream_destroy": [vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -99,7 +101,8 @@ _lib = _load_library()
 # Exported symbols of the C ABI (checked by the CPU tests against include/kvio.h).
 EXPORTS = ("kvio_pool_create", "kvio_pool_destroy", "kvio_load", "kvio_offload", "kvio_load_layer",
            "kvio_check", "kvio_naive_load", "kvio_naive_offload", "kvio_memcpy", "kvio_host_alloc",
-           "kvio_host_free", "kvio_strerror", "kvio_last_error")
+           "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_strerror",
+           "kvio_last_error")
 
 
 def kvio_strerror(status: int) -> str:
@@ -215,6 +218,43 @@ def kvio_host_alloc(nbytes: int, flags: int = KVIO_HOST_COHERENT) -> int:
 
 def kvio_host_free(ptr: int) -> None:
     _check(_lib.kvio_host_free(ptr))
+
+
+def kvio_stream_create(cu_mask=None) -> int:
+    """Raw hipStream_t (int).  cu_mask: None for an ordinary non-blocking stream,
+    or a sequence of CU indices the stream's kernels may use."""
+    out = ctypes.c_void_p()
+    if cu_mask is None:
+        _check(_lib.kvio_stream_create(None, 0, ctypes.byref(out)))
+    else:
+        cus = sorted(set(int(c) for c in cu_mask))
+        words = (ctypes.c_uint32 * (cus[-1] // 32 + 1 if cus else 1))()
+        for c in cus:
+            words[c // 32] |= 1 << (c % 32)
+        _check(_lib.kvio_stream_create(words, len(words), ctypes.byref(out)))
+    return out.value
+
+
+def kvio_stream_destroy(stream: int) -> None:
+    _check(_lib.kvio_stream_destroy(stream))
+
+
+class Stream:
+    """A kvio_stream_create stream wrapped for torch (torch.cuda.ExternalStream)."""
+
+    def __init__(self, cu_mask=None):
+        self.handle = kvio_stream_create(cu_mask)
+        self.torch = torch.cuda.ExternalStream(self.handle)
+
+    @property
+    def cuda_stream(self) -> int:
+        return self.handle
+
+    def close(self) -> None:
+        if self.handle:
+            torch.cuda.synchronize()
+            kvio_stream_destroy(self.handle)
+            self.handle = 0
 
 
 class HostBuffer:

@@ -11,3 +11,21 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an AMD Instinct GPU (gfx950) and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+@pytest.fixture(scope="session")
+def io_stream():
+    """One transfer stream with a hardware queue of its own (a CU mask over all
+    CUs), shared by every GPU test: ordinary streams share a few hardware queues
+    round-robin and can serialise, and the runtime allows few masked streams
+    per process.  Falls back to a torch stream if the runtime refuses."""
+    import torch
+    import paper_2508_18572_amd as kv
+    try:
+        n = torch.cuda.get_device_properties(0).multi_processor_count
+        st = kv.Stream(list(range(n)))
+    except kv.KvioError:
+        yield torch.cuda.Stream()
+        return
+    yield st.torch
+    st.close()

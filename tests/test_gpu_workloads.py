@@ -70,7 +70,7 @@ def test_workload1_tiny_pool_exact(kv):
         pool.close()
 
 
-def single_context_workload(kv, k, layerwise=False):
+def single_context_workload(kv, k, io_stream, layerwise=False):
     import torch
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -86,7 +86,7 @@ def single_context_workload(kv, k, layerwise=False):
         pool = kv.KVPool(pool_t, P)
         span = [(hb.ptr, T, T, pt.data_ptr())]
         if layerwise:
-            side = torch.cuda.Stream()
+            side = io_stream
             compute = torch.cuda.current_stream()
             for l in range(L):
                 ev = torch.cuda.Event()
@@ -108,12 +108,12 @@ def single_context_workload(kv, k, layerwise=False):
         pool.close()
 
 
-def test_workload2_llama8b_page1(kv):
-    single_context_workload(kv, 2)
+def test_workload2_llama8b_page1(kv, io_stream):
+    single_context_workload(kv, 2, io_stream)
 
 
-def test_workload3_70b_layerwise(kv):
-    single_context_workload(kv, 3, layerwise=True)
+def test_workload3_70b_layerwise(kv, io_stream):
+    single_context_workload(kv, 3, io_stream, layerwise=True)
 
 
 def test_workload4_batched_churned(kv):
@@ -174,7 +174,7 @@ def test_workload4_batched_churned(kv):
     pool.close()
 
 
-def test_workload5_1m_with_concurrent_offload(kv):
+def test_workload5_1m_with_concurrent_offload(kv, io_stream):
     """1M-token load at page size 1 on one stream while 16K other slots are
     offloaded repeatedly to a separate host chunk on a second stream."""
     import torch
@@ -196,7 +196,7 @@ def test_workload5_1m_with_concurrent_offload(kv):
         W.fill_cuda(src_o.ptr, nbo, W.data_seed(k) * 1000 + 1, shp)
         pool.load([(src_o.ptr, TO, TO, po.data_ptr())])          # set-up: resident data to offload
         torch.cuda.synchronize()
-        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+        sa, sb = io_stream, torch.cuda.Stream()
         done = torch.cuda.Event()
         pool.load([(hb.ptr, T, T, pl.data_ptr())], stream=sa)
         done.record(sa)
