@@ -32,6 +32,10 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 # of the oracle (to show that the pins catch plausible mistakes).
 _LIB_PATH = os.environ.get("KVO_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
+TOKEN_MAJOR = 0
+PAGE_FIRST = 1
+HEAD_MAJOR = 2
+
 OK = 0
 EINVAL = -1
 ERANGE = -2
@@ -72,6 +76,14 @@ def _load():
         f = getattr(lib, name)
         f.restype = ctypes.c_int
         f.argtypes = [vp, vp, i32, i64, i32, i64, i32, vp, vp, vp, vp, i32, i32]
+    for name in ("kvo_load_layout", "kvo_offload_layout"):
+        f = getattr(lib, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [vp, vp, i32, i64, i32, i64, i32, i32, i32, vp, vp, vp, vp, i32, i32]
+    lib.kvo_host_row_offset_page_first.restype = i64
+    lib.kvo_host_row_offset_page_first.argtypes = [i32, i32, i32, i32, i64, i64]
+    lib.kvo_host_seg_offset_head_major.restype = i64
+    lib.kvo_host_seg_offset_head_major.argtypes = [i32, i32, i32, i32, i64, i64, i64]
     _lib = lib
     return lib
 
@@ -88,6 +100,26 @@ def _check(rc: int, what: str) -> None:
 def host_row_offset(layer: int, kv: int, host_tokens: int, token: int, row_bytes: int) -> int:
     """Byte offset of host row (layer, kv, token) in a layer-major chunk."""
     return int(_load().kvo_host_row_offset(layer, kv, host_tokens, token, row_bytes))
+
+
+def host_row_offset_page_first(layer: int, kv: int, num_layers: int, page_size: int, token: int,
+                               row_bytes: int) -> int:
+    """Byte offset of host row (layer, kv, token) in a page-first chunk."""
+    return int(_load().kvo_host_row_offset_page_first(layer, kv, num_layers, page_size, token, row_bytes))
+
+
+def host_seg_offset_head_major(layer: int, kv: int, head: int, num_heads: int, host_tokens: int, token: int,
+                               seg_bytes: int) -> int:
+    """Byte offset of head `head` of row (layer, kv, token) in a head-major chunk."""
+    return int(_load().kvo_host_seg_offset_head_major(layer, kv, head, num_heads, host_tokens, token,
+                                                        seg_bytes))
+
+
+def host_chunk_bytes(layout: int, num_layers: int, host_tokens: int, row_bytes: int, page_size: int) -> int:
+    """Bytes of one context's host chunk in a layout."""
+    if layout == PAGE_FIRST:
+        return -(-host_tokens // page_size) * page_size * num_layers * 2 * row_bytes
+    return num_layers * 2 * host_tokens * row_bytes
 
 
 def expand_slots(page_idx: np.ndarray, page_size: int, num_tokens: int, num_slots: int) -> np.ndarray:
@@ -130,7 +162,8 @@ def _layer_ptrs(pool: np.ndarray):
     return (ctypes.c_void_p * pool.shape[0])(*[_ptr(pool[i]) for i in range(pool.shape[0])])
 
 
-def _batch(fn, k_pool, v_pool, page_size, spans: Sequence[Span], layer_begin, layer_end, what):
+def _batch(fn, k_pool, v_pool, page_size, spans: Sequence[Span], layer_begin, layer_end, what,
+           layout=None, num_heads=1):
     assert k_pool.shape == v_pool.shape
     num_layers, num_slots, row_bytes = k_pool.shape
     n = len(spans)
@@ -141,15 +174,19 @@ def _batch(fn, k_pool, v_pool, page_size, spans: Sequence[Span], layer_begin, la
     ntok = np.zeros(max(n, 1), dtype=np.int64)
     for i, (host, host_tokens, num_tokens, page_idx) in enumerate(spans):
         assert host.dtype == np.uint8 and host.flags.c_contiguous
-        assert host.size >= num_layers * 2 * host_tokens * row_bytes
+        assert host.size >= host_chunk_bytes(layout or TOKEN_MAJOR, num_layers, host_tokens, row_bytes, page_size)
         p = np.ascontiguousarray(page_idx, dtype=np.int32)
         keep.append(p)
         hosts[i] = _ptr(host)
         pidxs[i] = _ptr(p) if p.size else None
         htok[i] = host_tokens
         ntok[i] = num_tokens
-    rc = fn(_layer_ptrs(k_pool), _layer_ptrs(v_pool), num_layers, num_slots, page_size, row_bytes,
-            n, hosts, _ptr(htok), _ptr(ntok), pidxs, layer_begin, layer_end)
+    if layout is None:
+        rc = fn(_layer_ptrs(k_pool), _layer_ptrs(v_pool), num_layers, num_slots, page_size, row_bytes,
+                n, hosts, _ptr(htok), _ptr(ntok), pidxs, layer_begin, layer_end)
+    else:
+        rc = fn(_layer_ptrs(k_pool), _layer_ptrs(v_pool), num_layers, num_slots, page_size, row_bytes,
+                num_heads, layout, n, hosts, _ptr(htok), _ptr(ntok), pidxs, layer_begin, layer_end)
     _check(rc, what)
 
 
@@ -166,3 +203,19 @@ def offload(k_pool: np.ndarray, v_pool: np.ndarray, page_size: int, spans: Itera
     layer_end = k_pool.shape[0] if layer_end is None else layer_end
     _batch(_load().kvo_offload_batch, k_pool, v_pool, page_size, list(spans), layer_begin, layer_end,
            "offload")
+
+
+def load_layout(k_pool: np.ndarray, v_pool: np.ndarray, page_size: int, spans: Iterable[Span], layout: int,
+                num_heads: int = 1, layer_begin: int = 0, layer_end: int | None = None) -> None:
+    """Load host chunks in any layout (TOKEN_MAJOR, PAGE_FIRST, HEAD_MAJOR)."""
+    layer_end = k_pool.shape[0] if layer_end is None else layer_end
+    _batch(_load().kvo_load_layout, k_pool, v_pool, page_size, list(spans), layer_begin, layer_end,
+           "load_layout", layout, num_heads)
+
+
+def offload_layout(k_pool: np.ndarray, v_pool: np.ndarray, page_size: int, spans: Iterable[Span], layout: int,
+                   num_heads: int = 1, layer_begin: int = 0, layer_end: int | None = None) -> None:
+    """Offload into host chunks in any layout."""
+    layer_end = k_pool.shape[0] if layer_end is None else layer_end
+    _batch(_load().kvo_offload_layout, k_pool, v_pool, page_size, list(spans), layer_begin, layer_end,
+           "offload_layout", layout, num_heads)

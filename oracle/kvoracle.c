@@ -37,6 +37,22 @@
 #include <stdlib.h>
 #include <string.h>
 
+/*
+ * Host chunk layouts.  All three hold the same rows; they differ only in where
+ * row (l, kv, t) -- or, head-major, its head h segment -- sits in the chunk:
+ *   TOKEN_MAJOR (layer-major chunk per context):
+ *       ((l*2 + kv)*host_tokens + t) * R
+ *   PAGE_FIRST (Sec. 4.2.1, Fig. 6: the layers of one page stored together, the
+ *   transfer-friendly layout for host and disk; host_tokens is a multiple of P):
+ *       (((t/P)*L + l)*2 + kv) * P*R + (t%P) * R
+ *   HEAD_MAJOR (one contiguous run per (layer, K|V, head); the segment of head h
+ *   of row t, De = head_dim * element bytes bytes long):
+ *       (((l*2 + kv)*H + h)*host_tokens + t) * De
+ */
+#define KVO_TOKEN_MAJOR 0
+#define KVO_PAGE_FIRST 1
+#define KVO_HEAD_MAJOR 2
+
 #define KVO_OK 0
 #define KVO_EINVAL (-1)   /* bad sizes, null pointers, num_tokens > host_tokens */
 #define KVO_ERANGE (-2)   /* a page index outside [0, S/P)                       */
@@ -48,6 +64,22 @@ int64_t kvo_host_row_offset(int32_t layer, int32_t kv, int64_t host_tokens,
                             int64_t token, int64_t row_bytes)
 {
     return (((int64_t)layer * 2 + kv) * host_tokens + token) * row_bytes;
+}
+
+/* Page-first layout: byte offset of host row (layer, kv, token). */
+int64_t kvo_host_row_offset_page_first(int32_t layer, int32_t kv, int32_t num_layers,
+                                       int32_t page_size, int64_t token, int64_t row_bytes)
+{
+    int64_t page = token / page_size;
+    int64_t in_page = token % page_size;
+    return (((page * num_layers + layer) * 2 + kv) * page_size + in_page) * row_bytes;
+}
+
+/* Head-major layout: byte offset of the head `head` segment of row (layer, kv, token). */
+int64_t kvo_host_seg_offset_head_major(int32_t layer, int32_t kv, int32_t head, int32_t num_heads,
+                                       int64_t host_tokens, int64_t token, int64_t seg_bytes)
+{
+    return ((((int64_t)layer * 2 + kv) * num_heads + head) * host_tokens + token) * seg_bytes;
 }
 
 /*
@@ -246,4 +278,92 @@ int kvo_offload_batch(const uint8_t *const *k_pool, const uint8_t *const *v_pool
         }
     }
     return KVO_OK;
+}
+
+/*
+ * Load / offload for any host layout.  `num_heads` is H (R = H * seg bytes);
+ * for PAGE_FIRST, host_tokens must be a multiple of the page size.  Same
+ * validation and semantics as kvo_load_batch / kvo_offload_batch.
+ */
+static int kvo_move_layout(uint8_t *const *k_pool, uint8_t *const *v_pool, int32_t num_layers,
+                           int64_t num_slots, int32_t page_size, int64_t row_bytes, int32_t num_heads,
+                           int32_t host_layout, int32_t n_spans, uint8_t *const *host,
+                           const int64_t *host_tokens, const int64_t *num_tokens,
+                           const int32_t *const *page_idx, int32_t layer_begin, int32_t layer_end,
+                           int to_pool)
+{
+    int32_t s, l, kv, h;
+    int64_t t;
+    int rc;
+    int64_t seg;
+    if (k_pool == NULL || v_pool == NULL || row_bytes <= 0 || num_heads < 1 ||
+        row_bytes % num_heads != 0 || layer_begin < 0 || layer_end > num_layers ||
+        layer_begin >= layer_end)
+        return KVO_EINVAL;
+    if (host_layout != KVO_TOKEN_MAJOR && host_layout != KVO_PAGE_FIRST && host_layout != KVO_HEAD_MAJOR)
+        return KVO_EINVAL;
+    if (n_spans > 0 && (host == NULL || host_tokens == NULL || num_tokens == NULL || page_idx == NULL))
+        return KVO_EINVAL;
+    rc = kvo_check_batch(n_spans, host_tokens, num_tokens, page_idx, num_slots, page_size, to_pool);
+    if (rc != KVO_OK)
+        return rc;
+    seg = row_bytes / num_heads;
+    for (s = 0; s < n_spans; ++s) {
+        if (num_tokens[s] == 0)
+            continue;
+        if (host[s] == NULL)
+            return KVO_EINVAL;
+        if (host_layout == KVO_PAGE_FIRST && host_tokens[s] % page_size != 0)
+            return KVO_EINVAL;
+        for (l = layer_begin; l < layer_end; ++l) {
+            for (kv = 0; kv < 2; ++kv) {
+                uint8_t *slab = kv == 0 ? k_pool[l] : v_pool[l];
+                for (t = 0; t < num_tokens[s]; ++t) {
+                    int64_t slot = (int64_t)page_idx[s][t / page_size] * page_size + t % page_size;
+                    uint8_t *prow = slab + slot * row_bytes;
+                    if (host_layout == KVO_HEAD_MAJOR) {
+                        for (h = 0; h < num_heads; ++h) {
+                            uint8_t *hseg = host[s] + kvo_host_seg_offset_head_major(
+                                                          l, kv, h, num_heads, host_tokens[s], t, seg);
+                            if (to_pool)
+                                memcpy(prow + h * seg, hseg, (size_t)seg);
+                            else
+                                memcpy(hseg, prow + h * seg, (size_t)seg);
+                        }
+                    } else {
+                        int64_t off = host_layout == KVO_TOKEN_MAJOR
+                            ? kvo_host_row_offset(l, kv, host_tokens[s], t, row_bytes)
+                            : kvo_host_row_offset_page_first(l, kv, num_layers, page_size, t, row_bytes);
+                        if (to_pool)
+                            memcpy(prow, host[s] + off, (size_t)row_bytes);
+                        else
+                            memcpy(host[s] + off, prow, (size_t)row_bytes);
+                    }
+                }
+            }
+        }
+    }
+    return KVO_OK;
+}
+
+int kvo_load_layout(uint8_t *const *k_pool, uint8_t *const *v_pool, int32_t num_layers,
+                    int64_t num_slots, int32_t page_size, int64_t row_bytes, int32_t num_heads,
+                    int32_t host_layout, int32_t n_spans, const uint8_t *const *host,
+                    const int64_t *host_tokens, const int64_t *num_tokens,
+                    const int32_t *const *page_idx, int32_t layer_begin, int32_t layer_end)
+{
+    return kvo_move_layout(k_pool, v_pool, num_layers, num_slots, page_size, row_bytes, num_heads,
+                           host_layout, n_spans, (uint8_t *const *)host, host_tokens, num_tokens,
+                           page_idx, layer_begin, layer_end, 1);
+}
+
+int kvo_offload_layout(uint8_t *const *k_pool, uint8_t *const *v_pool, int32_t num_layers,
+                       int64_t num_slots, int32_t page_size, int64_t row_bytes, int32_t num_heads,
+                       int32_t host_layout, int32_t n_spans, uint8_t *const *host,
+                       const int64_t *host_tokens, const int64_t *num_tokens,
+                       const int32_t *const *page_idx, int32_t layer_begin, int32_t layer_end)
+{
+    return kvo_move_layout(k_pool, v_pool, num_layers, num_slots, page_size, row_bytes, num_heads,
+                           host_layout, n_spans, host, host_tokens, num_tokens, page_idx,
+                           layer_begin, layer_end, 0);
 }

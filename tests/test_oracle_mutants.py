@@ -43,6 +43,18 @@ MUTANTS = [
     ("no_duplicate_check",
      "if (written[slot / 8] & (uint8_t)(1u << (slot % 8))) {",
      "if (0) {", None),
+    ("page_first_layer_page_swapped",
+     "return (((page * num_layers + layer) * 2 + kv) * page_size + in_page) * row_bytes;",
+     "return (((layer * num_layers + page) * 2 + kv) * page_size + in_page) * row_bytes;", None),
+    ("page_first_in_page_dropped",
+     "return (((page * num_layers + layer) * 2 + kv) * page_size + in_page) * row_bytes;",
+     "return (((page * num_layers + layer) * 2 + kv) * page_size) * row_bytes;", None),
+    ("head_major_head_token_swapped",
+     "return ((((int64_t)layer * 2 + kv) * num_heads + head) * host_tokens + token) * seg_bytes;",
+     "return ((((int64_t)layer * 2 + kv) * host_tokens + token) * num_heads + head) * seg_bytes;", None),
+    ("head_major_pool_segment_offset_dropped",
+     "memcpy(prow + h * seg, hseg, (size_t)seg);",
+     "memcpy(prow, hseg, (size_t)seg);", None),
     ("layer_end_inclusive_check",
      "layer_end > num_layers || layer_begin >= layer_end)\n        return KVO_EINVAL;\n    if (n_spans > 0 && (host == NULL || host_tokens == NULL || num_tokens == NULL || page_idx == NULL))\n        return KVO_EINVAL;\n    rc = kvo_check_batch(n_spans, host_tokens, num_tokens, page_idx, num_slots, page_size, 1);",
      "layer_end > num_layers + 1 || layer_begin > layer_end)\n        return KVO_EINVAL;\n    if (n_spans > 0 && (host == NULL || host_tokens == NULL || num_tokens == NULL || page_idx == NULL))\n        return KVO_EINVAL;\n    rc = kvo_check_batch(n_spans, host_tokens, num_tokens, page_idx, num_slots, page_size, 1);", None),
@@ -61,6 +73,7 @@ def test_pins_catch_mutant(tmp_path, name, old, new, occ):
     subprocess.run(["gcc", "-std=c99", "-O1", "-fPIC", "-shared", str(c), "-o", str(lib)], check=True)
     env = dict(os.environ, KVO_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_layouts.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
