@@ -72,13 +72,29 @@ typedef enum kvio_status {
     KVIO_ENOMEM = -6       /* allocation failed                                              */
 } kvio_status;
 
-/* Host chunk layouts.  Only the layer-major, token-major layout above exists. */
+/* Host chunk layouts (kvio_pool_desc.host_layout).  All hold the same rows;
+ * they differ in where row (l, kv, t) -- head-major: its head h segment of
+ * De = head_dim * elem_bytes bytes -- starts inside one context's chunk:
+ *   KVIO_HOST_TOKEN_MAJOR  layer-major, K before V, token-major (above):
+ *                          ((l*2 + kv)*host_tokens + t) * R
+ *   KVIO_HOST_PAGE_FIRST   the paper's transfer-friendly layout (Sec. 4.2.1,
+ *                          Fig. 6): all layers of one context page together,
+ *                          [page][L][2][P][H][D]; host_tokens must be a
+ *                          multiple of P:  (((t/P)*L + l)*2 + kv)*P*R + (t%P)*R
+ *   KVIO_HOST_HEAD_MAJOR   one run per (layer, K|V, head), [L][2][H][T][D]:
+ *                          (((l*2 + kv)*H + h)*host_tokens + t) * De;
+ *                          De must be a multiple of 16.  Converting it to
+ *                          the token-major pool is a head/token transpose,
+ *                          staged through LDS unless KVIO_LAUNCH_NO_LDS. */
 #define KVIO_HOST_TOKEN_MAJOR 0
+#define KVIO_HOST_PAGE_FIRST 1
+#define KVIO_HOST_HEAD_MAJOR 2
 
 /* Launch shaping (Sec. 4.2: a small number of large workgroups keeps the I/O
  * kernel on few compute units; cache bypass limits pollution).  Zero fields
  * take the library defaults.  Results never depend on these. */
 #define KVIO_LAUNCH_CACHED 0x1     /* plain loads/stores instead of non-temporal ones */
+#define KVIO_LAUNCH_NO_LDS 0x2     /* head-major chunks: gather directly, no LDS staging */
 typedef struct kvio_launch {
     int32_t workgroups;   /* workgroups per launch, >= 1; 0 = default                       */
     int32_t threads;      /* threads per workgroup: multiple of 64 in [64, 1024]; 0 = default */
@@ -93,7 +109,7 @@ typedef struct kvio_pool_desc {
     int32_t head_dim;         /* D >= 1                                                  */
     int32_t elem_bytes;       /* bytes per element (2 for fp16/bf16); R % 16 must be 0  */
     int32_t page_size;        /* P >= 1 tokens                                           */
-    int32_t host_layout;      /* KVIO_HOST_TOKEN_MAJOR                                   */
+    int32_t host_layout;      /* KVIO_HOST_TOKEN_MAJOR | _PAGE_FIRST | _HEAD_MAJOR       */
     int64_t num_slots;        /* S token slots per per-layer pool, S % P == 0, S < 2^31 */
     void *const *k_layers;    /* host array of L device pointers, each S * R bytes       */
     void *const *v_layers;    /* host array of L device pointers, each S * R bytes       */
@@ -106,7 +122,7 @@ typedef struct kvio_pool *kvio_pool_t;
 /* One cached context (one "span" of a batched transfer). */
 typedef struct kvio_span {
     void *host;               /* pinned, device-mapped host chunk (or device memory),
-                                 16-byte aligned, >= L * 2 * host_tokens * R bytes     */
+                                 16-byte aligned, L * 2 * host_tokens * R bytes        */
     int64_t host_tokens;      /* token capacity of the chunk: its per-(layer, K|V) stride */
     int64_t num_tokens;       /* move context tokens [0, num_tokens); <= host_tokens     */
     const int32_t *page_idx;  /* DEVICE int32[ceil(num_tokens / P)]                      */

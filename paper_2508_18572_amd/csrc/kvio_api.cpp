@@ -47,8 +47,8 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // reach 90% of it on a 2 MiB context, and leave 240 of 256 CUs to co-running
 // compute.  Offload: 32 workgroups x 4 waves with 16 KiB steps (55.6 GB/s).
 constexpr int kDefaultThreads = 256;
-constexpr kvio::Shape kDefaultLoad = {16, kDefaultThreads, 4, true};
-constexpr kvio::Shape kDefaultOffload = {32, kDefaultThreads, 16, true};
+constexpr kvio::Shape kDefaultLoad = {16, kDefaultThreads, 4, true, true};
+constexpr kvio::Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
 
 kvio::Shape resolve(const kvio_launch &l, const kvio::Shape &def) {
     kvio::Shape s;
@@ -56,6 +56,7 @@ kvio::Shape resolve(const kvio_launch &l, const kvio::Shape &def) {
     s.threads = l.threads > 0 ? l.threads : def.threads;
     s.tile_kib = l.tile_kib > 0 ? l.tile_kib : def.tile_kib;
     s.nontemporal = (l.flags & KVIO_LAUNCH_CACHED) == 0;
+    s.head_major_lds = (l.flags & KVIO_LAUNCH_NO_LDS) == 0;
     return s;
 }
 
@@ -66,7 +67,7 @@ kvio_status check_launch(const kvio_launch &l, const char *which) {
         return fail(KVIO_EINVAL, "%s: threads %d is not a multiple of 64 in [64, 1024]", which, l.threads);
     if (l.tile_kib != 0 && l.tile_kib != 4 && l.tile_kib != 8 && l.tile_kib != 16)
         return fail(KVIO_EINVAL, "%s: tile_kib %d is not 4, 8 or 16", which, l.tile_kib);
-    if ((l.flags & ~KVIO_LAUNCH_CACHED) != 0)
+    if ((l.flags & ~(KVIO_LAUNCH_CACHED | KVIO_LAUNCH_NO_LDS)) != 0)
         return fail(KVIO_EINVAL, "%s: unknown launch flags 0x%x", which, l.flags);
     return KVIO_OK;
 }
@@ -121,6 +122,9 @@ kvio_status device_view(const void *p, uint64_t bytes, bool want_device_memory, 
 struct kvio_pool {
     int device;
     int32_t num_layers;
+    int32_t num_heads;
+    int32_t host_layout;
+    int64_t seg_bytes;               // head_dim * elem_bytes
     int32_t page_size;
     int64_t num_slots;
     int64_t row_bytes;
@@ -154,8 +158,12 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
     if (d->num_layers < 1 || d->num_kv_heads < 1 || d->head_dim < 1 || d->elem_bytes < 1 ||
         d->page_size < 1)
         return fail(KVIO_EINVAL, "kvio_pool_create: sizes must be >= 1");
-    if (d->host_layout != KVIO_HOST_TOKEN_MAJOR)
+    if (d->host_layout != KVIO_HOST_TOKEN_MAJOR && d->host_layout != KVIO_HOST_PAGE_FIRST &&
+        d->host_layout != KVIO_HOST_HEAD_MAJOR)
         return fail(KVIO_EINVAL, "kvio_pool_create: unknown host layout %d", d->host_layout);
+    if (d->host_layout == KVIO_HOST_HEAD_MAJOR && (int64_t(d->head_dim) * d->elem_bytes) % 16 != 0)
+        return fail(KVIO_EALIGN, "kvio_pool_create: head-major chunks need head_dim * elem_bytes (%lld) to be "
+                    "a multiple of 16", (long long)(int64_t(d->head_dim) * d->elem_bytes));
     if (d->num_slots < 1 || d->num_slots > INT32_MAX || d->num_slots % d->page_size != 0)
         return fail(KVIO_EINVAL, "kvio_pool_create: num_slots %lld must be in [1, 2^31) and a multiple "
                     "of page_size %d", (long long)d->num_slots, d->page_size);
@@ -174,6 +182,9 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
     kvio_pool *p = new (std::nothrow) kvio_pool();
     if (p == nullptr) return fail(KVIO_ENOMEM, "kvio_pool_create: host allocation failed");
     p->num_layers = d->num_layers;
+    p->num_heads = d->num_kv_heads;
+    p->host_layout = d->host_layout;
+    p->seg_bytes = int64_t(d->head_dim) * d->elem_bytes;
     p->page_size = d->page_size;
     p->num_slots = d->num_slots;
     p->row_bytes = R;
@@ -274,9 +285,25 @@ kvio_status validate(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
             if (!aligned16(s.host)) return fail(KVIO_EALIGN, "%s: span %d: host chunk not 16-byte aligned", fn, i);
             if ((reinterpret_cast<uintptr_t>(s.page_idx) & 3u) != 0)
                 return fail(KVIO_EALIGN, "%s: span %d: page table not 4-byte aligned", fn, i);
-            // Highest host byte the transfer touches: row (l1 - 1, V, num_tokens - 1).
-            const uint64_t reach = (uint64_t(l1 - 1) * 2 + 1) * uint64_t(s.host_tokens) * uint64_t(R) +
-                                   uint64_t(s.num_tokens) * uint64_t(R);
+            // One past the highest host byte the transfer can touch.
+            uint64_t reach;
+            const uint64_t P = uint64_t(p->page_size);
+            if (p->host_layout == KVIO_HOST_PAGE_FIRST) {
+                if (s.host_tokens % p->page_size != 0)
+                    return fail(KVIO_EINVAL, "%s: span %d: page-first chunks need host_tokens (%lld) to be a "
+                                "multiple of the page size %d", fn, i, (long long)s.host_tokens, p->page_size);
+                // whole pages up to the one holding token num_tokens - 1
+                reach = (uint64_t(s.num_tokens) + P - 1) / P * uint64_t(p->num_layers) * 2 * P * uint64_t(R);
+            } else if (p->host_layout == KVIO_HOST_HEAD_MAJOR) {
+                // segment (l1 - 1, V, H - 1, num_tokens - 1)
+                reach = ((uint64_t(l1 - 1) * 2 + 1) * uint64_t(p->num_heads) + uint64_t(p->num_heads) - 1) *
+                            uint64_t(s.host_tokens) * uint64_t(p->seg_bytes) +
+                        uint64_t(s.num_tokens) * uint64_t(p->seg_bytes);
+            } else {
+                // row (l1 - 1, V, num_tokens - 1)
+                reach = (uint64_t(l1 - 1) * 2 + 1) * uint64_t(s.host_tokens) * uint64_t(R) +
+                        uint64_t(s.num_tokens) * uint64_t(R);
+            }
             kvio_status st = device_view(s.host, reach, false, "host chunk", &r.host);
             if (st != KVIO_OK) return st;
             const int64_t pages = (s.num_tokens + p->page_size - 1) / p->page_size;
@@ -299,6 +326,9 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
     const kvio_launch &lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
     kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kDefaultLoad : kDefaultOffload);
     const int64_t R = p->row_bytes;
+    // LDS staging of a head-major tile needs the whole tile (>= one row) in the
+    // wave's U KiB slice.
+    if (p->host_layout == KVIO_HOST_HEAD_MAJOR && R > int64_t(shape.tile_kib) * 1024) shape.head_major_lds = false;
     const int rpt = kvio::rows_per_tile(R, shape.tile_kib);
     for (int32_t first = 0; first < n; first += KVIO_MAX_SPANS_PER_LAUNCH) {
         const int32_t cnt = n - first < KVIO_MAX_SPANS_PER_LAUNCH ? n - first : KVIO_MAX_SPANS_PER_LAUNCH;
@@ -317,6 +347,9 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
         a.rows_per_tile = rpt;
         a.n_spans = cnt;
         a.span_base = first;
+        a.host_layout = p->host_layout;
+        a.num_heads = p->num_heads;
+        a.seg_vecs = static_cast<int32_t>(p->seg_bytes / 16);
         int64_t tiles = 0;
         for (int32_t i = 0; i < cnt; ++i) {
             const Resolved &r = rs[size_t(first + i)];
@@ -347,6 +380,8 @@ kvio_status run_naive(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t 
     std::vector<Resolved> rs;
     kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
     if (st != KVIO_OK) return st;
+    if (p->host_layout == KVIO_HOST_HEAD_MAJOR)
+        return fail(KVIO_EINVAL, "%s: the per-page copy baseline takes token-major or page-first chunks", fn);
     const int64_t R = p->row_bytes;
     const int64_t P = p->page_size;
     const int64_t num_pages = p->num_slots / P;
@@ -370,7 +405,9 @@ kvio_status run_naive(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t 
                 for (int64_t j = 0; j < pages; ++j) {
                     const int64_t rows = (j + 1) * P <= s.num_tokens ? P : s.num_tokens - j * P;
                     uint8_t *prow = pool + int64_t(table[size_t(j)]) * P * R;
-                    uint8_t *hrow = hrow0 + j * P * R;
+                    uint8_t *hrow = p->host_layout == KVIO_HOST_PAGE_FIRST
+                        ? host + ((j * p->num_layers + l) * 2 + kv) * P * R
+                        : hrow0 + j * P * R;
                     hipError_t e2 = dir == kvio::kLoad
                         ? hipMemcpyAsync(prow, hrow, size_t(rows * R), hipMemcpyHostToDevice, stream)
                         : hipMemcpyAsync(hrow, prow, size_t(rows * R), hipMemcpyDeviceToHost, stream);

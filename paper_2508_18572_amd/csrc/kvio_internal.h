@@ -43,7 +43,9 @@ struct CopyArgs {
     int32_t rows_per_tile;         // 1 .. 64
     int32_t n_spans;               // spans in this launch, 1 .. KVIO_MAX_SPANS_PER_LAUNCH
     int32_t span_base;             // index of spans[0] in the caller's span array
-    int32_t pad_;
+    int32_t host_layout;           // KVIO_HOST_*
+    int32_t num_heads;             // H (head-major chunks)
+    int32_t seg_vecs;              // De / 16, 16-byte vectors per head segment (head-major)
     int64_t tile_prefix[KVIO_MAX_SPANS_PER_LAUNCH + 1];
     SpanArg spans[KVIO_MAX_SPANS_PER_LAUNCH];
 };
@@ -56,6 +58,7 @@ struct Shape {
     int threads;
     int tile_kib;      // 4, 8 or 16: vectors of 16 B per lane per step
     bool nontemporal;
+    bool head_major_lds;  // head-major chunks: stage the transpose through LDS
 };
 
 // Rows per tile for a given step size: one step moves tile_kib KiB per wave.

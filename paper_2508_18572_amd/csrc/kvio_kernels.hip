@@ -90,8 +90,6 @@ __device__ __forceinline__ TileLoc locate(const CopyArgs &a, int64_t g) {
 
 // Lane r < nrows: pool slot of token t0 + r, or -1 for rows past the tile or
 // an out-of-range page (recorded once in the error word, never dereferenced).
-// Lane r < nrows: pool slot of token t0 + r, or -1 for rows past the tile or
-// an out-of-range page (recorded once in the error word, never dereferenced).
 __device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp, int span,
                                          int64_t t0, int nrows, int lane) {
     int slot = -1;
@@ -123,38 +121,76 @@ __device__ __forceinline__ int row_of(const CopyArgs &a, int v) {
     return a.vec_shift >= 0 ? (v >> a.vec_shift) : (v / a.vec_per_row);
 }
 
+// Lane r < nrows, page-first host chunk (the layers of one context page stored
+// together, Sec. 4.2.1 / Fig. 6): byte offset of row (layer, kv, t0 + r) from
+// the chunk start.  Rows of one page are contiguous; pages are L * 2 * P rows
+// apart.
+__device__ __forceinline__ int64_t lane_host_row_page_first(const CopyArgs &a, int layer, int kv,
+                                                            int64_t t0, int nrows, int lane) {
+    if (lane >= nrows) return 0;
+    const int64_t t = t0 + lane;
+    int64_t cpage, off;
+    if (a.page_shift >= 0) {
+        cpage = t >> a.page_shift;
+        off = t & (a.page_size - 1);
+    } else {
+        cpage = t / a.page_size;
+        off = t - cpage * a.page_size;
+    }
+    return (((cpage * a.num_layers + layer) * 2 + kv) * a.page_size + off) * a.row_bytes;
+}
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(v), lane);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32), lane);
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Host layouts handled by kvio_copy_kernel: the tile's rows are one contiguous
+// run (token-major chunk), or each row sits at its own offset (page-first).
+constexpr int kHostTokenMajor = KVIO_HOST_TOKEN_MAJOR;
+constexpr int kHostPageFirst = KVIO_HOST_PAGE_FIRST;
+
 // Loads never carry a mask, so a wave's U loads issue back to back and the
 // compiler can count them exactly (precise s_waitcnt before each store).  A
 // chunk that must not move (past the end of a tile, or a row whose page was
 // out of range) is read from the first bytes of the pool layer instead: in
 // bounds, in device memory, and discarded.  Stores run unmasked when every
 // chunk of the step is valid (the common case) and guarded otherwise.
+//
+// `host` is the first byte of the tile's rows for a token-major chunk and the
+// chunk start for a page-first chunk, where `hoff` is the lane's row offset.
 
 // WIDE rows (R a multiple of 1 KiB): each wave-wide access of 64 x 16 B lies
 // in one row, so the row, its slot (read from the owning lane with readlane)
 // and both base addresses are wave-uniform scalars; each lane adds only its
 // own 16-byte offset.
-template <int DIR, int U, bool NT>
+template <int DIR, int U, bool NT, int HL>
 __device__ __forceinline__ void step_wide(const CopyArgs &a, uint8_t *host, uint8_t *pool, int slot,
-                                          int base, int nvec, uint32_t lane_off) {
+                                          int64_t hoff, int base, int nvec, uint32_t lane_off) {
     const int64_t R = a.row_bytes;
     const int nk = (nvec - base) / 64;      // valid chunks in this step (uniform, >= 1)
     int64_t pool_off[U];                    // chunk k's byte offset in the pool layer, -1 = skip
+    int64_t host_off[U];                    // chunk k's byte offset from `host`
     bool all_ok = true;
 #pragma unroll
     for (int k = 0; k < U; ++k) {
         const int v0 = base + k * 64;
         const int r = row_of(a, v0);
+        const int c0 = v0 - r * a.vec_per_row;
         const int s = __builtin_amdgcn_readlane(slot, r & 63);
-        pool_off[k] = (k < nk && s >= 0) ? static_cast<int64_t>(s) * R + (v0 - r * a.vec_per_row) * 16
-                                         : -1;
+        pool_off[k] = (k < nk && s >= 0) ? static_cast<int64_t>(s) * R + c0 * 16 : -1;
+        if constexpr (HL == kHostPageFirst)
+            host_off[k] = readlane64(hoff, r & 63) + c0 * 16;
+        else
+            host_off[k] = static_cast<int64_t>(v0) * 16;
         all_ok = all_ok && pool_off[k] >= 0;
     }
     u32x4 buf[U];
     if (DIR == kLoad) {
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            const uint8_t *src = k < nk ? host + static_cast<int64_t>(base + k * 64) * 16 : pool;
+            const uint8_t *src = k < nk ? host + host_off[k] : pool;
             buf[k] = load16<NT>(src + lane_off);
         }
         if (all_ok) {
@@ -171,33 +207,37 @@ __device__ __forceinline__ void step_wide(const CopyArgs &a, uint8_t *host, uint
             buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0) + lane_off);
         if (all_ok) {
 #pragma unroll
-            for (int k = 0; k < U; ++k)
-                store16<NT>(host + static_cast<int64_t>(base + k * 64) * 16 + lane_off, buf[k]);
+            for (int k = 0; k < U; ++k) store16<NT>(host + host_off[k] + lane_off, buf[k]);
         } else {
 #pragma unroll
             for (int k = 0; k < U; ++k)
-                if (pool_off[k] >= 0)
-                    store16<NT>(host + static_cast<int64_t>(base + k * 64) * 16 + lane_off, buf[k]);
+                if (pool_off[k] >= 0) store16<NT>(host + host_off[k] + lane_off, buf[k]);
         }
     }
 }
 
 // NARROW rows (any R multiple of 16 B): a wave-wide access may span several
-// rows, so each lane fetches its row's slot from the owning lane with a
-// cross-lane permute (ds_bpermute).
-template <int DIR, int U, bool NT>
+// rows, so each lane fetches its row's slot (and, page-first, its row's host
+// offset) from the owning lane with a cross-lane permute (ds_bpermute).
+template <int DIR, int U, bool NT, int HL>
 __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, uint8_t *pool, int slot,
-                                            int base, int nvec, int lane) {
+                                            int64_t hoff, int base, int nvec, int lane) {
     const int64_t R = a.row_bytes;
     const int V = a.vec_per_row;
     int64_t pool_off[U];                    // this lane's vector k offset in the pool layer, -1 = skip
+    int64_t host_off[U];                    // and its offset from `host`
     bool ok = true;
 #pragma unroll
     for (int k = 0; k < U; ++k) {
         const int j = base + k * 64 + lane;
         const int r = row_of(a, j);
+        const int c = j - r * V;
         const int s = __shfl(slot, r & 63);
-        pool_off[k] = (j < nvec && s >= 0) ? static_cast<int64_t>(s) * R + (j - r * V) * 16 : -1;
+        pool_off[k] = (j < nvec && s >= 0) ? static_cast<int64_t>(s) * R + c * 16 : -1;
+        if constexpr (HL == kHostPageFirst)
+            host_off[k] = __shfl(static_cast<long long>(hoff), r & 63) + c * 16;
+        else
+            host_off[k] = static_cast<int64_t>(j) * 16;
         ok = ok && pool_off[k] >= 0;
     }
     const bool all_ok = __all(ok);          // wave-uniform
@@ -206,7 +246,7 @@ __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, ui
 #pragma unroll
         for (int k = 0; k < U; ++k) {
             const int j = base + k * 64 + lane;
-            buf[k] = load16<NT>(j < nvec ? host + static_cast<int64_t>(j) * 16 : pool);
+            buf[k] = load16<NT>(j < nvec ? host + host_off[k] : pool);
         }
         if (all_ok) {
 #pragma unroll
@@ -221,21 +261,26 @@ __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, ui
         for (int k = 0; k < U; ++k) buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0));
         if (all_ok) {
 #pragma unroll
-            for (int k = 0; k < U; ++k)
-                store16<NT>(host + static_cast<int64_t>(base + k * 64 + lane) * 16, buf[k]);
+            for (int k = 0; k < U; ++k) store16<NT>(host + host_off[k], buf[k]);
         } else {
 #pragma unroll
             for (int k = 0; k < U; ++k)
-                if (pool_off[k] >= 0) store16<NT>(host + static_cast<int64_t>(base + k * 64 + lane) * 16, buf[k]);
+                if (pool_off[k] >= 0) store16<NT>(host + host_off[k], buf[k]);
         }
     }
 }
 
 // DIR: kLoad (host chunk -> pool) or kOffload (pool -> host chunk).
 // U: 16-byte vectors per lane per step (one step = U KiB per wave).
-// WIDE: R is a multiple of 1 KiB (see step_wide).
-template <int DIR, int U, bool NT, bool WIDE>
-__global__ void __launch_bounds__(1024) kvio_copy_kernel(const CopyArgs a) {
+// WIDE: R is a multiple of 1 KiB (see step_wide).  HL: host layout.
+// Workgroup size bound of the kernels that need more than 128 VGPRs per lane
+// (page-first and head-major addressing at 16 KiB steps); their launcher folds
+// larger workgroups into more workgroups of this size.
+constexpr int kNarrowBound = 256;
+
+template <int DIR, int U, bool NT, bool WIDE, int HL>
+__global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBound)
+    kvio_copy_kernel(const CopyArgs a) {
     const int lane = threadIdx.x & 63;
     const int waves_per_wg = blockDim.x >> 6;
     const int wave_in_wg = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -248,18 +293,160 @@ __global__ void __launch_bounds__(1024) kvio_copy_kernel(const CopyArgs a) {
         const TileLoc loc = locate(a, g);
         const SpanArg &sp = a.spans[loc.span];
         uint8_t *pool = a.layers[loc.kv * a.num_layers + loc.layer];
-        // First byte of the tile's rows inside the host chunk (layer-major, K then V).
-        uint8_t *host = const_cast<uint8_t *>(sp.host) +
-                        ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * sp.host_tokens + loc.t0) *
-                            a.row_bytes;
+        uint8_t *host = const_cast<uint8_t *>(sp.host);
+        int64_t hoff = 0;
+        if constexpr (HL == kHostPageFirst) {
+            hoff = lane_host_row_page_first(a, loc.layer, loc.kv, loc.t0, loc.nrows, lane);
+        } else {
+            // First byte of the tile's rows (layer-major chunk, K then V).
+            host += ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * sp.host_tokens + loc.t0) * a.row_bytes;
+        }
         const int slot = lane_slot(a, sp, loc.span, loc.t0, loc.nrows, lane);
         const int nvec = loc.nrows * a.vec_per_row;
 #pragma unroll 1
         for (int base = 0; base < nvec; base += 64 * U) {
             if constexpr (WIDE) {
-                step_wide<DIR, U, NT>(a, host, pool, slot, base, nvec, lane_off);
+                step_wide<DIR, U, NT, HL>(a, host, pool, slot, hoff, base, nvec, lane_off);
             } else {
-                step_narrow<DIR, U, NT>(a, host, pool, slot, base, nvec, lane);
+                step_narrow<DIR, U, NT, HL>(a, host, pool, slot, hoff, base, nvec, lane);
+            }
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------
+// Head-major host chunk: one contiguous run per (layer, K|V, head), so a pool
+// row (token-major [H][D]) gathers H segments of De = R / H bytes from H runs.
+// This is the head/token transpose of the layout conversion.
+//
+// LDS = true: each wave owns one tile of n rows that fits its share of LDS.
+// It reads the tile in host order (per head, n * De contiguous bytes), writes
+// each 16-byte vector to its pool-order position in the wave's LDS slice,
+// and then reads the slice back in pool order, so both sides are long
+// contiguous runs: host reads of n * De bytes, pool writes of whole rows.
+// Offload runs the same two phases the other way round.
+// LDS = false: a direct gather in pool order (each wave-wide access reads
+// 64 / (De / 16) head segments of De bytes from as many runs).
+//
+// Vector numbering inside a tile (Vd = De / 16 vectors per segment,
+// V = H * Vd per row):
+//   pool order  p = r * V + h * Vd + c     (pool row r, head h, vector c)
+//   host order  q = (h * n + r) * Vd + c
+// ----------------------------------------------------------------------------
+template <int DIR, int U, bool NT, bool LDS>
+__global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const CopyArgs a) {
+    extern __shared__ u32x4 lds[];           // U * 64 vectors per wave
+    const int lane = threadIdx.x & 63;
+    const int waves_per_wg = blockDim.x >> 6;
+    const int wave_in_wg = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * waves_per_wg;
+    u32x4 *slice = lds + wave_in_wg * (U * 64);
+    const int64_t R = a.row_bytes;
+    const int V = a.vec_per_row;
+    const int Vd = a.seg_vecs;
+    const int64_t De = static_cast<int64_t>(Vd) * 16;
+
+#pragma unroll 1
+    for (int64_t g = static_cast<int64_t>(blockIdx.x) * waves_per_wg + wave_in_wg;
+         g < a.total_tiles; g += nwaves) {
+        const TileLoc loc = locate(a, g);
+        const SpanArg &sp = a.spans[loc.span];
+        uint8_t *pool = a.layers[loc.kv * a.num_layers + loc.layer];
+        const int n = loc.nrows;
+        // Start of head 0's run at token t0; head h's run is h * host_tokens * De further.
+        uint8_t *host = const_cast<uint8_t *>(sp.host) +
+                        ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * a.num_heads * sp.host_tokens + loc.t0) * De;
+        const int64_t head_stride = sp.host_tokens * De;
+        const int slot = lane_slot(a, sp, loc.span, loc.t0, n, lane);
+        const int nvec = n * V;
+#pragma unroll 1
+        for (int base = 0; base < nvec; base += 64 * U) {
+            if constexpr (LDS) {
+                // The whole tile is one step (rows_per_tile keeps n * R <= U KiB).
+                if (DIR == kLoad) {
+                    u32x4 buf[U];
+#pragma unroll
+                    for (int k = 0; k < U; ++k) {          // host order, contiguous per head
+                        const int q = k * 64 + lane;
+                        const int hr = q / Vd;              // h * n + r
+                        const int h = hr / n;
+                        const int r = hr - h * n;
+                        const int c = q - hr * Vd;
+                        buf[k] = load16<NT>(q < nvec ? host + h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16
+                                                     : pool);
+                        if (q < nvec) slice[r * V + h * Vd + c] = buf[k];
+                    }
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+                    for (int k = 0; k < U; ++k) {          // pool order, whole rows
+                        const int p = k * 64 + lane;
+                        const int r = p / V;
+                        const int s = __shfl(slot, r & 63);
+                        if (p < nvec && s >= 0)
+                            store16<NT>(pool + static_cast<int64_t>(s) * R + (p - r * V) * 16, slice[p]);
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < U; ++k) {          // pool order, whole rows
+                        const int p = k * 64 + lane;
+                        const int r = p / V;
+                        const int s = __shfl(slot, r & 63);
+                        const u32x4 v = load16<NT>(pool + (p < nvec && s >= 0
+                                                               ? static_cast<int64_t>(s) * R + (p - r * V) * 16
+                                                               : 0));
+                        if (p < nvec) slice[p] = v;
+                    }
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+                    for (int k = 0; k < U; ++k) {          // host order, contiguous per head
+                        const int q = k * 64 + lane;
+                        const int hr = q / Vd;
+                        const int h = hr / n;
+                        const int r = hr - h * n;
+                        const int c = q - hr * Vd;
+                        const int s = __shfl(slot, r & 63);
+                        if (q < nvec && s >= 0)
+                            store16<NT>(host + h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16,
+                                        slice[r * V + h * Vd + c]);
+                    }
+                }
+                // The slice is reused by the wave's next tile.
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            } else {
+                u32x4 buf[U];
+                int64_t pool_off[U];
+                int64_t host_off[U];
+#pragma unroll
+                for (int k = 0; k < U; ++k) {              // pool order
+                    const int p = base + k * 64 + lane;
+                    const int r = p / V;
+                    const int hv = p - r * V;
+                    const int h = hv / Vd;
+                    const int c = hv - h * Vd;
+                    const int s = __shfl(slot, r & 63);
+                    pool_off[k] = (p < nvec && s >= 0) ? static_cast<int64_t>(s) * R + hv * 16 : -1;
+                    host_off[k] = h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16;
+                }
+                if (DIR == kLoad) {
+#pragma unroll
+                    for (int k = 0; k < U; ++k)
+                        buf[k] = load16<NT>(base + k * 64 + lane < nvec ? host + host_off[k] : pool);
+#pragma unroll
+                    for (int k = 0; k < U; ++k)
+                        if (pool_off[k] >= 0) store16<NT>(pool + pool_off[k], buf[k]);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < U; ++k) buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0));
+#pragma unroll
+                    for (int k = 0; k < U; ++k)
+                        if (pool_off[k] >= 0) store16<NT>(host + host_off[k], buf[k]);
+                }
             }
         }
     }
@@ -272,12 +459,31 @@ int rows_per_tile(int64_t row_bytes, int tile_kib) {
 
 template <int DIR, int U, bool NT>
 static hipError_t launch_u(const CopyArgs &a, const Shape &s, hipStream_t stream) {
-    if (a.vec_per_row % 64 == 0) {
-        hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, true>), dim3(s.workgroups), dim3(s.threads),
-                           0, stream, a);
-    } else {
-        hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, false>), dim3(s.workgroups), dim3(s.threads),
-                           0, stream, a);
+    dim3 grid(s.workgroups), block(s.threads);
+    const bool wide = a.vec_per_row % 64 == 0;
+    if (a.host_layout != KVIO_HOST_TOKEN_MAJOR && s.threads > kNarrowBound) {
+        grid = dim3(static_cast<unsigned>(int64_t(s.workgroups) * s.threads / kNarrowBound));
+        block = dim3(kNarrowBound);
+    }
+    switch (a.host_layout) {
+        case kHostPageFirst:
+            if (wide)
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, true, kHostPageFirst>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, false, kHostPageFirst>), grid, block, 0, stream, a);
+            break;
+        case KVIO_HOST_HEAD_MAJOR:
+            if (s.head_major_lds)
+                hipLaunchKernelGGL((kvio_head_major_kernel<DIR, U, NT, true>), grid, block,
+                                   static_cast<size_t>(block.x / 64) * U * 1024, stream, a);
+            else
+                hipLaunchKernelGGL((kvio_head_major_kernel<DIR, U, NT, false>), grid, block, 0, stream, a);
+            break;
+        default:
+            if (wide)
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, true, kHostTokenMajor>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, false, kHostTokenMajor>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }

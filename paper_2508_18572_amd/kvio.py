@@ -31,7 +31,10 @@ KVIO_EHIP = -5
 KVIO_ENOMEM = -6
 
 KVIO_HOST_TOKEN_MAJOR = 0
+KVIO_HOST_PAGE_FIRST = 1
+KVIO_HOST_HEAD_MAJOR = 2
 KVIO_LAUNCH_CACHED = 0x1
+KVIO_LAUNCH_NO_LDS = 0x2
 KVIO_HOST_COHERENT = 0x0
 KVIO_HOST_NONCOHERENT = 0x1
 KVIO_MAX_SPANS_PER_LAUNCH = 64
@@ -284,7 +287,8 @@ class KVPool:
     layer a token-major (S, H, D) array of 16-bit elements."""
 
     def __init__(self, pool: "torch.Tensor", page_size: int,
-                 load_launch: Optional[kvio_launch] = None, offload_launch: Optional[kvio_launch] = None):
+                 load_launch: Optional[kvio_launch] = None, offload_launch: Optional[kvio_launch] = None,
+                 host_layout: int = KVIO_HOST_TOKEN_MAJOR):
         assert pool.is_cuda and pool.is_contiguous() and pool.dim() == 5 and pool.shape[0] == 2
         _, L, S, H, D = pool.shape
         self.tensor = pool
@@ -293,7 +297,7 @@ class KVPool:
         self.handle = kvio_pool_create(L, H, D, pool.element_size(), page_size, S,
                                        [pool[0, l].data_ptr() for l in range(L)],
                                        [pool[1, l].data_ptr() for l in range(L)],
-                                       load_launch, offload_launch)
+                                       load_launch, offload_launch, host_layout)
 
     def load(self, spans, layer_begin=0, layer_end=None, stream=None):
         kvio_load(self.handle, spans, layer_begin, self.num_layers if layer_end is None else layer_end, stream)
