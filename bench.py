@@ -58,6 +58,9 @@ def parse():
                     help="workgroups,threads,tile_kib of the background offload that runs beside a load "
                          "(the bidirectional workload); a small quota, as the paper gives backups")
     ap.add_argument("--noncoherent-host", action="store_true", help="coarse-grained pinned host chunks")
+    ap.add_argument("--host-layout", choices=["token", "page", "head"], default="token",
+                    help="host chunk layout: token-major (default), page-first, or head-major")
+    ap.add_argument("--no-lds", action="store_true", help="head-major chunks: direct gather, no LDS staging")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-peak", action="store_true")
@@ -270,7 +273,13 @@ def h2d_d2h_peak(torch, kv, nbytes=2 << 30):
 
 
 def launch_from(args, kv):
-    return kv.launch(args.workgroups, args.threads, args.tile_kib, kv.KVIO_LAUNCH_CACHED if args.cached else 0)
+    flags = (kv.KVIO_LAUNCH_CACHED if args.cached else 0) | (kv.KVIO_LAUNCH_NO_LDS if args.no_lds else 0)
+    return kv.launch(args.workgroups, args.threads, args.tile_kib, flags)
+
+
+def layout_from(args, kv):
+    return {"token": kv.KVIO_HOST_TOKEN_MAJOR, "page": kv.KVIO_HOST_PAGE_FIRST,
+            "head": kv.KVIO_HOST_HEAD_MAJOR}[args.host_layout]
 
 
 def run_layerwise(args, torch, kv, W):
@@ -291,7 +300,7 @@ def run_layerwise(args, torch, kv, W):
     host = kv.HostBuffer(nbytes)
     peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
     W.fill_cuda(host.ptr, nbytes, W.data_seed(k), shp)
-    pool = kv.KVPool(pool_t, P, load_launch=launch_from(args, kv))
+    pool = kv.KVPool(pool_t, P, load_launch=launch_from(args, kv), host_layout=layout_from(args, kv))
     span = [(host.ptr, T, T, pidx.data_ptr())]
     side, comp = io_stream(torch, kv), torch.cuda.Stream()
     M, N, K = 4096, 8192, 8192
@@ -641,8 +650,8 @@ def run_single(args, torch, kv, W, k):
     W.fill_cuda(host.ptr, host_bytes, W.data_seed(k), shp)
     log(f"host chunk {host_bytes / 2**30:.2f} GiB filled in {time.perf_counter() - t0:.1f}s")
 
-    launch = kv.launch(args.workgroups, args.threads, args.tile_kib, kv.KVIO_LAUNCH_CACHED if args.cached else 0)
-    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
+    launch = launch_from(args, kv)
+    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch, host_layout=layout_from(args, kv))
     span_in = [(host.ptr, T, T, pidx.data_ptr())]
     span_out = [(out.ptr, T, T, pidx.data_ptr())]
     stream = io_stream(torch, kv)
@@ -683,7 +692,7 @@ def run_single(args, torch, kv, W, k):
 
     # ---- naive per-page DMA baseline (prefix of the calls) -------------------------------
     naive = None
-    if not args.no_naive:
+    if not args.no_naive and args.host_layout != "head":
         nt = min(T, args.naive_tokens)
         nt -= nt % P if nt > P else 0
         spn = [(host.ptr, T, nt, pidx.data_ptr())]
@@ -706,7 +715,7 @@ def run_single(args, torch, kv, W, k):
 
     # ---- CPU oracle baseline --------------------------------------------------------------
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.host_layout == "token":
         nbytes, el, passes = cpu_baseline(S, R, host.array, T, T, pages, P, L, args.cpu_seconds)
         cpu = {"value": nbytes / el / GB, "unit": "GB/s", "cores": 1, "kind": "oracle",
                "sample": f"{passes} pass(es) of load+offload of the whole {T}-token context, one "
@@ -721,7 +730,8 @@ def run_single(args, torch, kv, W, k):
         log(f"steady state over 1000 loads: {steady['load_gbps']:.2f} GB/s, single shot "
             f"{steady['single_shot_us']:.1f} us; same-size memcpy {steady['memcpy_gbps']:.2f} GB/s")
 
-    default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host)
+    default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host
+                          or args.no_lds or args.host_layout != "token")
     traffic = measured_traffic(k, default_launch)
     frac_h2d = load_gbps / peak["h2d"] if peak else None
     frac_d2h = off_gbps / peak["d2h"] if peak else None
@@ -746,6 +756,7 @@ def run_single(args, torch, kv, W, k):
                    "launch": {"workgroups": args.workgroups or "default", "threads": args.threads or "default",
                               "tile_kib": args.tile_kib or "default", "nontemporal": not args.cached},
                    "host_memory": "non-coherent" if args.noncoherent_host else "coherent",
+                   "host_layout": args.host_layout + ("" if not args.no_lds else " (no LDS)"),
                    "io_stream": _IO.get("kind")},
         "tokens_per_s": round(2 * T / (step_ms * 1e-3), 1),
         "load": {"ms": round(load_ms, 4), "gbps": round(load_gbps, 3), "tokens_per_s": round(T / (load_ms * 1e-3), 1),

@@ -365,6 +365,7 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
                 // The whole tile is one step (rows_per_tile keeps n * R <= U KiB).
                 if (DIR == kLoad) {
                     u32x4 buf[U];
+                    int pos[U];                             // pool-order position of vector q, -1 = none
 #pragma unroll
                     for (int k = 0; k < U; ++k) {          // host order, contiguous per head
                         const int q = k * 64 + lane;
@@ -372,10 +373,14 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
                         const int h = hr / n;
                         const int r = hr - h * n;
                         const int c = q - hr * Vd;
+                        pos[k] = q < nvec ? r * V + h * Vd + c : -1;
                         buf[k] = load16<NT>(q < nvec ? host + h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16
                                                      : pool);
-                        if (q < nvec) slice[r * V + h * Vd + c] = buf[k];
                     }
+                    // All U loads are in flight before the first LDS write waits for one.
+#pragma unroll
+                    for (int k = 0; k < U; ++k)
+                        if (pos[k] >= 0) slice[pos[k]] = buf[k];
                     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                     __builtin_amdgcn_wave_barrier();
                     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -388,16 +393,19 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
                             store16<NT>(pool + static_cast<int64_t>(s) * R + (p - r * V) * 16, slice[p]);
                     }
                 } else {
+                    u32x4 buf[U];
 #pragma unroll
                     for (int k = 0; k < U; ++k) {          // pool order, whole rows
                         const int p = k * 64 + lane;
                         const int r = p / V;
                         const int s = __shfl(slot, r & 63);
-                        const u32x4 v = load16<NT>(pool + (p < nvec && s >= 0
-                                                               ? static_cast<int64_t>(s) * R + (p - r * V) * 16
-                                                               : 0));
-                        if (p < nvec) slice[p] = v;
+                        buf[k] = load16<NT>(pool + (p < nvec && s >= 0
+                                                        ? static_cast<int64_t>(s) * R + (p - r * V) * 16
+                                                        : 0));
                     }
+#pragma unroll
+                    for (int k = 0; k < U; ++k)
+                        if (k * 64 + lane < nvec) slice[k * 64 + lane] = buf[k];
                     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                     __builtin_amdgcn_wave_barrier();
                     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
