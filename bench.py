@@ -65,6 +65,10 @@ def parse():
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-peak", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--interference", action="store_true",
+                    help="resource-quota sweep (Strata Fig. 5 analogue): load GB/s and the slowdown of a "
+                         "co-running prefill-like GEMM and decode-like HBM-bound kernel vs. the load's "
+                         "workgroup quota, on the Llama-3.1-8B page-size-1 workload")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="only run a plain device-to-device elementwise copy of this many bytes, three "
                          "times (the known-size kernel that scales the HBM byte counters), then exit")
@@ -589,6 +593,108 @@ def run_bidirectional(args, torch, kv, W):
     print(json.dumps(res), flush=True)
 
 
+def run_interference(args, torch, kv, W):
+    """Load bandwidth and co-runner slowdown vs. the load kernel's quota.
+
+    Stand-ins for the paper's co-runners (Fig. 5): a prefill-like bf16 GEMM
+    (two 4K-token requests through a Llama-3.1-8B MLP up-projection,
+    8192 x 4096 x 14336) and a decode-like HBM-bound pass (reading the KV of 16
+    requests x 4K tokens of the 8B shape, 8 GiB, as one reduction).  The
+    co-runner loops on its own stream while one 4 GiB kvio_load runs on the
+    transfer stream; iterations that lie inside the load's window give the
+    co-run time per iteration."""
+    k = 2
+    wl = W.WORKLOADS[k]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    pages = W.random_slots(np.random.default_rng(W.placement_seed(k)), S, T)
+    pidx = torch.from_numpy(pages).cuda()
+    nb = L * 2 * T * R
+    host = kv.HostBuffer(nb)
+    W.fill_cuda(host.ptr, nb, W.data_seed(k), shp)
+    io, comp = io_stream(torch, kv), torch.cuda.Stream()
+    span = [(host.ptr, T, T, pidx.data_ptr())]
+    g = torch.Generator(device="cuda").manual_seed(7)
+    A = torch.randn(8192, 4096, device="cuda", dtype=torch.bfloat16, generator=g)
+    B = torch.randn(4096, 14336, device="cuda", dtype=torch.bfloat16, generator=g)
+    C = torch.empty(8192, 14336, device="cuda", dtype=torch.bfloat16)
+    kvbuf = torch.randn(4 << 30, device="cuda", dtype=torch.bfloat16, generator=g)   # 8 GiB
+    red = torch.empty((), device="cuda", dtype=torch.float32)
+    corunners = {
+        "prefill_gemm": lambda: torch.matmul(A, B, out=C),
+        "decode_hbm": lambda: torch.sum(kvbuf, dim=(0,), dtype=torch.float32, out=red),
+    }
+
+    def alone(fn, n=20):
+        ts = []
+        for _ in range(n):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(comp)
+            with torch.cuda.stream(comp):
+                fn()
+            b.record(comp)
+            ts.append((a, b))
+        torch.cuda.synchronize()
+        return statistics.median(x.elapsed_time(y) for x, y in ts)
+
+    def load_alone(pool):
+        pool.load(span, stream=io)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(io)
+        pool.load(span, stream=io)
+        b.record(io)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    quotas = [(1, 1024), (2, 1024), (4, 1024), (2, 256), (4, 256), (8, 256), (16, 256), (32, 256),
+              (64, 256), (128, 256), (32, 64), (64, 64), (128, 64), (256, 64), (64, 128), (128, 128)]
+    rows = []
+    base = {name: alone(fn) for name, fn in corunners.items()}
+    log(f"co-runners alone: " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
+    for wg, th in quotas:
+        pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
+        row = {"workgroups": wg, "threads": th, "waves": wg * th // 64,
+               "load_gbps_alone": round(nb / (load_alone(pool) * 1e-3) / GB, 3)}
+        for name, fn in corunners.items():
+            n_iter = int(200 / base[name]) + 20            # enough to outlast the load
+            torch.cuda.synchronize()
+            start = torch.cuda.Event(enable_timing=True)
+            start.record(comp)
+            marks = []
+            with torch.cuda.stream(comp):
+                for _ in range(n_iter):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(comp)
+                    fn()
+                    b.record(comp)
+                    marks.append((a, b))
+            io.wait_event(marks[5][0])                      # the co-runner is already running
+            l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            l0.record(io)
+            pool.load(span, stream=io)
+            l1.record(io)
+            torch.cuda.synchronize()
+            t0, t1 = start.elapsed_time(l0), start.elapsed_time(l1)
+            inside = [x.elapsed_time(y) for x, y in marks
+                      if start.elapsed_time(x) >= t0 and start.elapsed_time(y) <= t1]
+            row[f"load_gbps_with_{name}"] = round(nb / ((t1 - t0) * 1e-3) / GB, 3)
+            row[f"{name}_slowdown"] = round(statistics.median(inside) / base[name], 4) if inside else None
+        pool.close()
+        rows.append(row)
+        log(f"quota {wg:3d} x {th:4d}: " + ", ".join(f"{k2} {v}" for k2, v in row.items()
+                                                    if k2 not in ("workgroups", "threads")))
+    res = base_result(args, max(r["load_gbps_alone"] for r in rows), 0.0,
+                      "interference sweep on config2: Llama-3.1-8B KV, page size 1, 32K-token load",
+                      {"corunners": {"prefill_gemm": [8192, 4096, 14336], "decode_hbm_bytes": 8 << 30},
+                       "corunner_ms_alone": {n: round(t, 4) for n, t in base.items()}})
+    res["sweep"] = rows
+    host.free()
+    print(json.dumps(res), flush=True)
+
+
 EXTRA_MODES = {3: run_layerwise, 4: run_batched, 5: run_bidirectional}
 
 
@@ -616,7 +722,9 @@ def main():
         return
     k = args.config
     try:
-        if k in EXTRA_MODES:
+        if args.interference:
+            run_interference(args, torch, kv, W)
+        elif k in EXTRA_MODES:
             EXTRA_MODES[k](args, torch, kv, W)
         else:
             run_single(args, torch, kv, W, k)
