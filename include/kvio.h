@@ -205,6 +205,51 @@ kvio_status kvio_host_free(void *ptr);
 kvio_status kvio_stream_create(const uint32_t *cu_mask, uint32_t mask_words, hipStream_t *out);
 kvio_status kvio_stream_destroy(hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Cache-aware batch formation (Sec. 4.3): the host-side step that decides
+ * which queued prefill requests the next batch loads and computes.
+ *
+ * One scheduling round:
+ *   1. Deferral on delay hit (Sec. 4.3.1): a request whose tokens match
+ *      transient (in-queue / in-flight) cache entries by more than
+ *      delay_hit_threshold tokens waits for the next round, at the front of
+ *      the queue.
+ *   2. Balanced batch formation (Sec. 4.3.2, Algorithm 1) over the others: the
+ *      queue head always joins, followed by every queued request that
+ *      bundle-hits the batch (reuses a context already in it; that context
+ *      is loaded once).  Then, while the batch is not full, requests are taken
+ *      in queue order: one that would make the batch loading-bound --
+ *      aggregated load tokens > loading_bound_ratio * aggregated compute
+ *      tokens, compared in double precision -- is deprioritized, otherwise it
+ *      joins and pulls in its own bundle hits.  Deprioritized requests then
+ *      fill any room left, in their original order.
+ * "Full" means the batch's compute tokens reached max_tokens or its size
+ * reached max_requests; as in Algorithm 1, a joining request is not checked
+ * against the remaining room.  The call is pure host code (no device work).
+ * ------------------------------------------------------------------------- */
+typedef struct kvio_request {
+    int64_t load_tokens;        /* cached tokens to load from host memory, >= 0           */
+    int64_t compute_tokens;     /* new tokens to prefill, >= 0                            */
+    int64_t context;            /* id of the cached context it reuses; < 0 = none         */
+    int64_t transient_matches;  /* tokens matched on in-queue / in-flight entries, >= 0   */
+} kvio_request;
+
+typedef struct kvio_batch_policy {
+    int64_t max_tokens;           /* token budget of a batch, >= 1                          */
+    int32_t max_requests;         /* request cap of a batch, >= 1                           */
+    int32_t reserved;             /* 0                                                      */
+    double loading_bound_ratio;   /* > 0; 0 = the paper's default 100; INFINITY = FIFO      */
+    int64_t delay_hit_threshold;  /* deferral threshold in matched tokens; < 0 = default 100 */
+} kvio_batch_policy;
+
+/* Form the next batch from `queue` (n requests, index 0 = head).  Writes the
+ * batch as queue indices in the order they joined to batch[0 .. *n_batch) and
+ * the next round's queue (deferred requests first, then the rest in queue
+ * order) to next_queue[0 .. *n_next); both arrays must hold n entries.
+ * n == 0 gives an empty batch.  KVIO_EINVAL on bad arguments. */
+kvio_status kvio_schedule_round(const kvio_request *queue, int32_t n, const kvio_batch_policy *policy,
+                                int32_t *batch, int32_t *n_batch, int32_t *next_queue, int32_t *n_next);
+
 /* Static text for a status code. */
 const char *kvio_strerror(kvio_status status);
 

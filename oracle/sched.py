@@ -24,8 +24,9 @@ Readings where the paper is silent (also listed in the design notes):
   * is_full: the batch's compute tokens reached the token budget, or its
     request count reached the request cap.  Like Algorithm 1, adding a request
     does not check the remaining room (the last one may overshoot).
-  * loading_bound(r): load(B + r) > ratio * compute(B + r); a batch with no
-    compute is loading-bound as soon as it has any load.
+  * loading_bound(r): load(B + r) > ratio * compute(B + r), compared in
+    double precision; a batch with no compute is loading-bound as soon as it
+    has any load.
   * Requests not placed in the batch keep their relative order; the next
     round's queue is: deferred delay hits (in order), then the rest.
 """
@@ -69,7 +70,8 @@ class Batch:
     def loading_bound(self, r: Request) -> bool:
         load = self.load + self.added_load(r)
         compute = self.compute + r.compute_tokens
-        return load > self.ratio * compute
+        # the decision is taken in double precision, as the library takes it
+        return float(load) > float(self.ratio) * float(compute)
 
     def add(self, r: Request) -> None:
         self.load += self.added_load(r)

@@ -7,7 +7,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvio.so")
-SOURCES = [os.path.join(CSRC, "kvio_kernels.hip"), os.path.join(CSRC, "kvio_api.cpp")]
+SOURCES = [os.path.join(CSRC, "kvio_kernels.hip"), os.path.join(CSRC, "kvio_api.cpp"),
+           os.path.join(CSRC, "kvio_sched.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

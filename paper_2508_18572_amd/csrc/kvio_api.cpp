@@ -119,6 +119,12 @@ kvio_status device_view(const void *p, uint64_t bytes, bool want_device_memory, 
 
 }  // namespace
 
+// Error path shared with kvio_sched.cpp (same thread-local error text).
+kvio_status kvio_sched_fail(kvio_status st, const char *msg) {
+    g_last_error.clear();
+    return fail(st, "%s", msg);
+}
+
 struct kvio_pool {
     int device;
     int32_t num_layers;

@@ -60,6 +60,17 @@ class kvio_span(ctypes.Structure):
                 ("num_tokens", ctypes.c_int64), ("page_idx", ctypes.c_void_p)]
 
 
+class kvio_request(ctypes.Structure):
+    _fields_ = [("load_tokens", ctypes.c_int64), ("compute_tokens", ctypes.c_int64),
+                ("context", ctypes.c_int64), ("transient_matches", ctypes.c_int64)]
+
+
+class kvio_batch_policy(ctypes.Structure):
+    _fields_ = [("max_tokens", ctypes.c_int64), ("max_requests", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("loading_bound_ratio", ctypes.c_double),
+                ("delay_hit_threshold", ctypes.c_int64)]
+
+
 class KvioError(RuntimeError):
     def __init__(self, status: int, detail: str):
         super().__init__(f"{kvio_strerror(status)}: {detail}")
@@ -87,6 +98,9 @@ def _load_library() -> ctypes.CDLL:
         "kvio_host_free": [vp],
         "kvio_stream_create": [ctypes.POINTER(ctypes.c_uint32), ctypes.c_uint32, ctypes.POINTER(vp)],
         "kvio_stream_destroy": [vp],
+        "kvio_schedule_round": [ctypes.POINTER(kvio_request), i32, ctypes.POINTER(kvio_batch_policy),
+                                ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                ctypes.POINTER(i32)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -104,8 +118,8 @@ _lib = _load_library()
 # Exported symbols of the C ABI (checked by the CPU tests against include/kvio.h).
 EXPORTS = ("kvio_pool_create", "kvio_pool_destroy", "kvio_load", "kvio_offload", "kvio_load_layer",
            "kvio_check", "kvio_naive_load", "kvio_naive_offload", "kvio_memcpy", "kvio_host_alloc",
-           "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_strerror",
-           "kvio_last_error")
+           "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_schedule_round",
+           "kvio_strerror", "kvio_last_error")
 
 
 def kvio_strerror(status: int) -> str:
@@ -258,6 +272,23 @@ class Stream:
             torch.cuda.synchronize()
             kvio_stream_destroy(self.handle)
             self.handle = 0
+
+
+def kvio_schedule_round(requests, max_tokens: int, max_requests: int, loading_bound_ratio: float = 0.0,
+                        delay_hit_threshold: int = -1):
+    """One scheduling round over `requests`, a sequence of (load_tokens,
+    compute_tokens, context or -1, transient_matches).  Returns (batch, next
+    queue) as lists of indices into `requests`."""
+    n = len(requests)
+    arr = (kvio_request * max(n, 1))()
+    for i, (load, comp, ctx, match) in enumerate(requests):
+        arr[i] = kvio_request(load, comp, -1 if ctx is None else ctx, match)
+    pol = kvio_batch_policy(max_tokens, max_requests, 0, loading_bound_ratio, delay_hit_threshold)
+    b = (ctypes.c_int32 * max(n, 1))()
+    q = (ctypes.c_int32 * max(n, 1))()
+    nb, nq = ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.kvio_schedule_round(arr, n, ctypes.byref(pol), b, ctypes.byref(nb), q, ctypes.byref(nq)))
+    return list(b[:nb.value]), list(q[:nq.value])
 
 
 class HostBuffer:

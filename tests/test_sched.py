@@ -1,0 +1,80 @@
+"""Batch formation in libkvio (kvio_schedule_round) against the oracle of
+Strata Sec. 4.3 / Algorithm 1, on the worked example and on many random
+queues.  Pure host code: runs without a GPU."""
+import math
+
+import hypothesis.strategies as st
+import pytest
+from hypothesis import HealthCheck, given, settings
+
+from oracle.sched import Request, schedule_round
+
+
+@pytest.fixture(scope="module")
+def kv():
+    import paper_2508_18572_amd as kv
+    return kv
+
+
+def run_both(kv, reqs, max_tokens, max_requests, ratio=100.0, thr=100):
+    oq = [Request(i, l, c, None if ctx < 0 else ctx, m) for i, (l, c, ctx, m) in enumerate(reqs)]
+    exp = schedule_round(oq, max_tokens, max_requests, ratio, thr)
+    got = kv.kvio_schedule_round(reqs, max_tokens, max_requests, ratio, thr)
+    assert got == (exp[0], exp[1]), (reqs, max_tokens, max_requests, ratio, thr)
+    return got
+
+
+def test_figure7(kv):
+    reqs = [(80_000, 1_000, 3, 0), (60_000, 200, 7, 0), (60_000, 200, 7, 0), (0, 2_000, -1, 0)]
+    assert run_both(kv, reqs, 8_000, 2) == ([0, 3], [1, 2])
+    # defaults (ratio 0 -> 100, threshold -1 -> 100) give the same round
+    assert kv.kvio_schedule_round(reqs, 8_000, 2) == ([0, 3], [1, 2])
+
+
+def test_edges(kv):
+    assert run_both(kv, [], 100, 4) == ([], [])
+    assert run_both(kv, [(0, 10, -1, 500)] * 3, 100, 4) == ([], [0, 1, 2])       # all deferred
+    run_both(kv, [(5, 0, -1, 0), (0, 0, -1, 0), (7, 0, 1, 0), (3, 0, 1, 0)], 1, 8)  # zero compute
+    run_both(kv, [(2**53 + 1, 2**40, -1, 0), (2**60, 2**44, 2, 0)], 2**62, 8, ratio=4096.0)
+    run_both(kv, [(10**6, 1, -1, 0)] * 5, 10, 8, ratio=math.inf)                  # FIFO
+
+
+request = st.tuples(st.sampled_from([0, 1, 50, 4096, 10**5, 10**7]), st.integers(0, 5000),
+                    st.integers(-1, 5), st.sampled_from([0, 0, 0, 99, 100, 101, 10**4]))
+
+
+@settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(st.lists(request, max_size=40), st.integers(1, 20_000), st.integers(1, 12),
+       st.sampled_from([0.5, 10.0, 100.0, 1000.0, math.inf]), st.sampled_from([0, 100, 10**9]))
+def test_random_queues_match_oracle(kv, reqs, max_tokens, max_requests, ratio, thr):
+    run_both(kv, reqs, max_tokens, max_requests, ratio, thr)
+
+
+def test_multi_round_drain(kv):
+    import random
+    rnd = random.Random(11)
+    reqs = [(rnd.choice([0, 10**4, 10**6]), rnd.randint(1, 4000), rnd.randint(-1, 6), rnd.choice([0, 0, 500]))
+            for _ in range(200)]
+    cur = list(range(200))
+    seen = []
+    for _ in range(400):
+        if not cur:
+            break
+        sub = [reqs[i] for i in cur]
+        # transient matches resolve once a round has passed (in-flight -> cached)
+        b, nxt = run_both(kv, sub, 8192, 16)
+        seen += [cur[i] for i in b]
+        cur = [cur[i] for i in nxt]
+        reqs = [(l, c, x, 0) for (l, c, x, m) in reqs]
+    assert sorted(seen) == list(range(200))
+
+
+def test_policy_validation(kv):
+    with pytest.raises(kv.KvioError):
+        kv.kvio_schedule_round([(1, 1, -1, 0)], 0, 4)
+    with pytest.raises(kv.KvioError):
+        kv.kvio_schedule_round([(1, 1, -1, 0)], 10, 0)
+    with pytest.raises(kv.KvioError):
+        kv.kvio_schedule_round([(-1, 1, -1, 0)], 10, 4)
+    with pytest.raises(kv.KvioError):
+        kv.kvio_schedule_round([(1, 1, -1, 0)], 10, 4, loading_bound_ratio=-1.0)
