@@ -69,7 +69,8 @@ typedef enum kvio_status {
     KVIO_EALIGN = -3,      /* R, a pool layer or a host chunk not 16-byte aligned            */
     KVIO_ENOTMAPPED = -4,  /* host chunk not accessible from the device (e.g. plain malloc)  */
     KVIO_EHIP = -5,        /* a HIP runtime call failed; its message is in kvio_last_error  */
-    KVIO_ENOMEM = -6       /* allocation failed                                              */
+    KVIO_ENOMEM = -6,      /* allocation failed                                              */
+    KVIO_EIO = -7          /* a disk read or write failed or came up short (errno in the text) */
 } kvio_status;
 
 /* Host chunk layouts (kvio_pool_desc.host_layout).  All hold the same rows;
@@ -204,6 +205,50 @@ kvio_status kvio_host_free(void *ptr);
  * synchronising it. */
 kvio_status kvio_stream_create(const uint32_t *cu_mask, uint32_t mask_words, hipStream_t *out);
 kvio_status kvio_stream_destroy(hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Storage tier (Sec. 4.2.1): cached contexts kept on disk are prefetched
+ * into pinned host chunks, from where kvio_load moves them to the pool; the
+ * reverse (kvio_disk_store_pages) backs a host chunk up to disk.  The paper
+ * stores host and disk copies page-first, so every page is one large
+ * contiguous transfer instead of L * 2 small ones (Fig. 12).
+ *
+ * A disk store is one file of KV pages of one model, P tokens per page,
+ * R = H * D * elem_bytes bytes per row, in one of two layouts:
+ *   KVIO_DISK_PAGE_FIRST   [disk page][L][2][P][H][D]: row (l, kv, o) of disk
+ *                          page p at byte ((p*L + l)*2 + kv)*P*R + o*R
+ *   KVIO_DISK_LAYER_FIRST  the pool's own order, [L][2][disk page][P][H][D]:
+ *                          at ((l*2 + kv)*num_disk_pages + p)*P*R + o*R
+ * Context page j (tokens [j*P, j*P + P)) lives in disk page disk_pages[j].
+ * Transfers copy whole pages: the host chunk (token-major or page-first host
+ * layout, see KVIO_HOST_*) must hold host_tokens >= n_pages * P tokens.
+ * Contiguous pieces are merged; `threads` positioned reads / writes run in
+ * parallel.  With an O_DIRECT descriptor every offset, length and address
+ * must be 4 KiB aligned (pinned host memory is).  Pure host code; the calls
+ * block until done.
+ * ------------------------------------------------------------------------- */
+#define KVIO_DISK_PAGE_FIRST 0
+#define KVIO_DISK_LAYER_FIRST 1
+typedef struct kvio_disk_store {
+    int32_t fd;               /* open file descriptor                              */
+    int32_t disk_layout;      /* KVIO_DISK_PAGE_FIRST | KVIO_DISK_LAYER_FIRST      */
+    int64_t num_disk_pages;   /* pages the file holds                              */
+    int32_t num_layers;       /* L                                                 */
+    int32_t page_size;        /* P tokens                                          */
+    int64_t row_bytes;        /* R                                                 */
+} kvio_disk_store;
+
+/* Read the n_pages disk pages of one context into `host` (host_layout
+ * KVIO_HOST_TOKEN_MAJOR or KVIO_HOST_PAGE_FIRST).  KVIO_EINVAL on bad
+ * arguments or a disk page outside [0, num_disk_pages); KVIO_EIO on a failed
+ * or short read. */
+kvio_status kvio_disk_prefetch(const kvio_disk_store *store, const int64_t *disk_pages, int32_t n_pages,
+                               void *host, int64_t host_tokens, int32_t host_layout, int32_t threads);
+
+/* Write the n_pages context pages of `host` to the disk pages (backup). */
+kvio_status kvio_disk_store_pages(const kvio_disk_store *store, const int64_t *disk_pages, int32_t n_pages,
+                                  const void *host, int64_t host_tokens, int32_t host_layout,
+                                  int32_t threads);
 
 /* ---------------------------------------------------------------------------
  * Cache-aware batch formation (Sec. 4.3): the host-side step that decides

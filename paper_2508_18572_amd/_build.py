@@ -8,7 +8,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvio.so")
 SOURCES = [os.path.join(CSRC, "kvio_kernels.hip"), os.path.join(CSRC, "kvio_api.cpp"),
-           os.path.join(CSRC, "kvio_sched.cpp")]
+           os.path.join(CSRC, "kvio_sched.cpp"), os.path.join(CSRC, "kvio_disk.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -17,7 +17,7 @@ FLAGS = [
     # keep the compiler from forming packed fp32 ops (there are no fp32 ops
     # here, but every HIP source of this project is built this way)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-I", INCLUDE, "-I", CSRC,
+    "-I", INCLUDE, "-I", CSRC, "-pthread",
 ]
 
 

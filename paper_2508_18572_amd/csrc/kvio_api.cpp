@@ -122,6 +122,7 @@ kvio_status device_view(const void *p, uint64_t bytes, bool want_device_memory, 
 // Error path shared with kvio_sched.cpp (same thread-local error text).
 kvio_status kvio_sched_fail(kvio_status st, const char *msg) {
     g_last_error.clear();
+    if (st == KVIO_OK) return KVIO_OK;
     return fail(st, "%s", msg);
 }
 
@@ -152,6 +153,7 @@ const char *kvio_strerror(kvio_status st) {
         case KVIO_ENOTMAPPED: return "KVIO_ENOTMAPPED: host memory not accessible from the device";
         case KVIO_EHIP: return "KVIO_EHIP: HIP runtime error";
         case KVIO_ENOMEM: return "KVIO_ENOMEM: out of memory";
+        case KVIO_EIO: return "KVIO_EIO: disk read or write failed";
     }
     return "unknown kvio_status";
 }

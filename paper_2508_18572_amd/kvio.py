@@ -35,6 +35,9 @@ KVIO_HOST_PAGE_FIRST = 1
 KVIO_HOST_HEAD_MAJOR = 2
 KVIO_LAUNCH_CACHED = 0x1
 KVIO_LAUNCH_NO_LDS = 0x2
+KVIO_EIO = -7
+KVIO_DISK_PAGE_FIRST = 0
+KVIO_DISK_LAYER_FIRST = 1
 KVIO_HOST_COHERENT = 0x0
 KVIO_HOST_NONCOHERENT = 0x1
 KVIO_MAX_SPANS_PER_LAUNCH = 64
@@ -71,6 +74,11 @@ class kvio_batch_policy(ctypes.Structure):
                 ("delay_hit_threshold", ctypes.c_int64)]
 
 
+class kvio_disk_store(ctypes.Structure):
+    _fields_ = [("fd", ctypes.c_int32), ("disk_layout", ctypes.c_int32), ("num_disk_pages", ctypes.c_int64),
+                ("num_layers", ctypes.c_int32), ("page_size", ctypes.c_int32), ("row_bytes", ctypes.c_int64)]
+
+
 class KvioError(RuntimeError):
     def __init__(self, status: int, detail: str):
         super().__init__(f"{kvio_strerror(status)}: {detail}")
@@ -98,6 +106,8 @@ def _load_library() -> ctypes.CDLL:
         "kvio_host_free": [vp],
         "kvio_stream_create": [ctypes.POINTER(ctypes.c_uint32), ctypes.c_uint32, ctypes.POINTER(vp)],
         "kvio_stream_destroy": [vp],
+        "kvio_disk_prefetch": [ctypes.POINTER(kvio_disk_store), ctypes.POINTER(i64), i32, vp, i64, i32, i32],
+        "kvio_disk_store_pages": [ctypes.POINTER(kvio_disk_store), ctypes.POINTER(i64), i32, vp, i64, i32, i32],
         "kvio_schedule_round": [ctypes.POINTER(kvio_request), i32, ctypes.POINTER(kvio_batch_policy),
                                 ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32),
                                 ctypes.POINTER(i32)],
@@ -119,6 +129,7 @@ _lib = _load_library()
 EXPORTS = ("kvio_pool_create", "kvio_pool_destroy", "kvio_load", "kvio_offload", "kvio_load_layer",
            "kvio_check", "kvio_naive_load", "kvio_naive_offload", "kvio_memcpy", "kvio_host_alloc",
            "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_schedule_round",
+           "kvio_disk_prefetch", "kvio_disk_store_pages",
            "kvio_strerror", "kvio_last_error")
 
 
@@ -289,6 +300,30 @@ def kvio_schedule_round(requests, max_tokens: int, max_requests: int, loading_bo
     nb, nq = ctypes.c_int32(), ctypes.c_int32()
     _check(_lib.kvio_schedule_round(arr, n, ctypes.byref(pol), b, ctypes.byref(nb), q, ctypes.byref(nq)))
     return list(b[:nb.value]), list(q[:nq.value])
+
+
+def _disk_args(fd, disk_layout, num_disk_pages, num_layers, page_size, row_bytes, disk_pages):
+    st = kvio_disk_store(fd, disk_layout, num_disk_pages, num_layers, page_size, row_bytes)
+    pages = (ctypes.c_int64 * max(len(disk_pages), 1))(*[int(p) for p in disk_pages])
+    return st, pages
+
+
+def kvio_disk_prefetch(fd: int, disk_layout: int, num_disk_pages: int, num_layers: int, page_size: int,
+                       row_bytes: int, disk_pages, host_ptr: int, host_tokens: int,
+                       host_layout: int = KVIO_HOST_TOKEN_MAJOR, threads: int = 8) -> None:
+    """Read a context's disk pages into the host chunk at host_ptr."""
+    st, pages = _disk_args(fd, disk_layout, num_disk_pages, num_layers, page_size, row_bytes, disk_pages)
+    _check(_lib.kvio_disk_prefetch(ctypes.byref(st), pages, len(disk_pages), host_ptr, host_tokens,
+                                   host_layout, threads))
+
+
+def kvio_disk_store_pages(fd: int, disk_layout: int, num_disk_pages: int, num_layers: int, page_size: int,
+                          row_bytes: int, disk_pages, host_ptr: int, host_tokens: int,
+                          host_layout: int = KVIO_HOST_TOKEN_MAJOR, threads: int = 8) -> None:
+    """Write a context's pages from the host chunk at host_ptr to the disk pages."""
+    st, pages = _disk_args(fd, disk_layout, num_disk_pages, num_layers, page_size, row_bytes, disk_pages)
+    _check(_lib.kvio_disk_store_pages(ctypes.byref(st), pages, len(disk_pages), host_ptr, host_tokens,
+                                      host_layout, threads))
 
 
 class HostBuffer:
