@@ -69,6 +69,11 @@ def parse():
                     help="resource-quota sweep (Strata Fig. 5 analogue): load GB/s and the slowdown of a "
                          "co-running prefill-like GEMM and decode-like HBM-bound kernel vs. the load's "
                          "workgroup quota, on the Llama-3.1-8B page-size-1 workload")
+    ap.add_argument("--disk", action="store_true",
+                    help="storage tier: 8192 tokens at page size 32 from a local disk store into pinned "
+                         "host memory, page-first vs layer-first, then into the paged pool")
+    ap.add_argument("--disk-dir", type=str, default=os.environ.get("TMPDIR", "/tmp"))
+    ap.add_argument("--disk-threads", type=str, default="1,8")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="only run a plain device-to-device elementwise copy of this many bytes, three "
                          "times (the known-size kernel that scales the HBM byte counters), then exit")
@@ -695,6 +700,136 @@ def run_interference(args, torch, kv, W):
     print(json.dumps(res), flush=True)
 
 
+def _open_store(path, direct):
+    """O_DIRECT when the filesystem takes it; otherwise a buffered descriptor
+    whose cached pages are dropped before every timed read."""
+    if direct:
+        try:
+            return os.open(path, os.O_RDONLY | os.O_DIRECT), True
+        except OSError:
+            pass
+    return os.open(path, os.O_RDONLY), False
+
+
+def run_disk(args, torch, kv, W):
+    """Fig. 12 analogue: latency of bringing 8192 cached tokens (page size 32)
+    of three models' KV from a local disk store into pinned host memory, with
+    the store and the host chunk page-first (one read of L*2*P*R bytes per
+    page) or layer-first (L*2 reads of P*R bytes per page), through O_DIRECT
+    descriptors (pinned chunks are then staged through bounce buffers) and
+    through buffered ones with the file's cached pages dropped before every
+    read.  The context's 256
+    pages sit at random disk pages of a 320-page store, so no two reads merge
+    by accident.  Both stores hold the same logical KV; after timing, the
+    layer-first store is also read into a page-first chunk (pieces of P*R) and
+    must equal the page-first result, and the two chunks loaded into the
+    layer-first paged pool (kvio_load, host layout to match) must give equal
+    pools."""
+    P, T = 32, 8192
+    n_ctx = T // P
+    N = n_ctx + n_ctx // 4
+    threads = [int(x) for x in args.disk_threads.split(",")]
+    reps = 3
+    rows = []
+    os.makedirs(args.disk_dir, exist_ok=True)
+    for si, shp in enumerate([W.LLAMA8B, W.GQA70B, W.QWEN7B1M]):
+        L, H, D, R = shp.num_layers, shp.num_kv_heads, shp.head_dim, shp.row_bytes
+        piece = P * R
+        page_bytes = L * 2 * piece
+        rng = np.random.default_rng(400 + si)
+        t0 = time.perf_counter()
+        logical = np.frombuffer(rng.bytes(N * page_bytes), np.uint8).reshape(N, L * 2, piece)
+        paths = {0: os.path.join(args.disk_dir, f"kv_store_page_first_{si}.bin"),
+                 1: os.path.join(args.disk_dir, f"kv_store_layer_first_{si}.bin")}
+        for lay, arr in ((0, logical), (1, np.ascontiguousarray(logical.transpose(1, 0, 2)))):
+            with open(paths[lay], "wb") as f:
+                arr.tofile(f)
+                f.flush()
+                os.fsync(f.fileno())
+        del logical
+        log(f"{shp.name}: two {N * page_bytes / 2**30:.2f} GiB stores written in {time.perf_counter() - t0:.1f}s")
+        disk_pages = rng.permutation(N)[:n_ctx]
+        nb = L * 2 * T * R
+        host_layout = {0: kv.KVIO_HOST_PAGE_FIRST, 1: kv.KVIO_HOST_TOKEN_MAJOR}
+        bufs = {0: kv.HostBuffer(nb), 1: kv.HostBuffer(nb)}
+        row = {"model": shp.name, "L": L, "R": R, "context_bytes": nb,
+               "reads_per_page": {"page_first": 1, "layer_first": L * 2},
+               "read_bytes": {"page_first": page_bytes, "layer_first": piece}}
+        try:
+            for lay, name in ((0, "page_first"), (1, "layer_first")):
+                for want_direct in (True, False):
+                    fd, direct = _open_store(paths[lay], want_direct)
+                    if want_direct and not direct:
+                        os.close(fd)
+                        continue
+                    mode = "direct" if direct else "buffered"
+                    try:
+                        for th in threads:
+                            ts = []
+                            for _ in range(reps):
+                                if not direct:
+                                    os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+                                t0 = time.perf_counter()
+                                kv.kvio_disk_prefetch(fd, lay, N, L, P, R, disk_pages, bufs[lay].ptr, T,
+                                                      host_layout[lay], th)
+                                ts.append(time.perf_counter() - t0)
+                            ms = statistics.median(ts) * 1e3
+                            row[f"{name}_{mode}_ms_t{th}"] = round(ms, 2)
+                            row[f"{name}_{mode}_gbps_t{th}"] = round(nb / (ms * 1e-3) / GB, 3)
+                    finally:
+                        os.close(fd)
+            for mode in ("direct", "buffered"):
+                for th in threads:
+                    if f"page_first_{mode}_ms_t{th}" in row:
+                        row[f"speedup_{mode}_t{th}"] = round(row[f"layer_first_{mode}_ms_t{th}"]
+                                                             / row[f"page_first_{mode}_ms_t{th}"], 2)
+            # same logical KV: the layer-first store read into a page-first chunk equals the page-first read
+            with kv.HostBuffer(nb) as chk:
+                fd, _ = _open_store(paths[1], True)
+                try:
+                    kv.kvio_disk_prefetch(fd, 1, N, L, P, R, disk_pages, chk.ptr, T, kv.KVIO_HOST_PAGE_FIRST, 8)
+                finally:
+                    os.close(fd)
+                row["cross_layout_equal"] = bool(np.array_equal(chk.array, bufs[0].array))
+            # on to the GPU: both chunks into the same layer-first pool layout
+            S = 2 * T
+            pidx = torch.from_numpy(W.random_pages(rng, S // P, n_ctx)).cuda()
+            pools = []
+            for lay in (0, 1):
+                pool_t = torch.zeros((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+                pool = kv.KVPool(pool_t, P, host_layout=host_layout[lay])
+                span = [(bufs[lay].ptr, T, T, pidx.data_ptr())]
+                pool.load(span)
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                pool.load(span)
+                b.record()
+                torch.cuda.synchronize()
+                pool.check()
+                row[f"{('page_first', 'layer_first')[lay]}_gpu_load_ms"] = round(a.elapsed_time(b), 3)
+                pool.close()
+                pools.append(pool_t)
+            row["pools_equal"] = bool(torch.equal(pools[0].view(torch.int16), pools[1].view(torch.int16)))
+            del pools
+        finally:
+            for b in bufs.values():
+                b.free()
+            for pth in paths.values():
+                os.remove(pth)
+        log(", ".join(f"{k2} {v}" for k2, v in row.items()))
+        rows.append(row)
+        if not (row["cross_layout_equal"] and row["pools_equal"]):
+            raise SystemExit(f"storage tier check failed for {shp.name}")
+    best = max(v for r in rows for k2, v in r.items() if k2.startswith("page_first_") and "_gbps_" in k2)
+    res = base_result(args, best, 0.0,
+                      "storage tier: 8192 tokens, page size 32, disk -> pinned host (page-first vs layer-first) "
+                      "-> paged pool", {"disk_threads": threads, "store_pages": N, "context_pages": n_ctx})
+    res["metric"] = "disk -> host GB/s of a cached context, page-first vs layer-first store"
+    res["sweep"] = rows
+    print(json.dumps(res), flush=True)
+
+
 EXTRA_MODES = {3: run_layerwise, 4: run_batched, 5: run_bidirectional}
 
 
@@ -724,6 +859,8 @@ def main():
     try:
         if args.interference:
             run_interference(args, torch, kv, W)
+        elif args.disk:
+            run_disk(args, torch, kv, W)
         elif k in EXTRA_MODES:
             EXTRA_MODES[k](args, torch, kv, W)
         else:

@@ -223,9 +223,14 @@ kvio_status kvio_stream_destroy(hipStream_t stream);
  * Transfers copy whole pages: the host chunk (token-major or page-first host
  * layout, see KVIO_HOST_*) must hold host_tokens >= n_pages * P tokens.
  * Contiguous pieces are merged; `threads` positioned reads / writes run in
- * parallel.  With an O_DIRECT descriptor every offset, length and address
- * must be 4 KiB aligned (pinned host memory is).  Pure host code; the calls
- * block until done.
+ * parallel.  With an O_DIRECT descriptor every file offset and length must
+ * be a multiple of the device's logical block size (P * R a multiple of
+ * 4 KiB is always enough).  Host memory that the OS cannot pin for direct I/O
+ * -- the HIP runtime's pinned allocations among it -- makes a direct transfer
+ * fail with EFAULT; the call then stages the rest through 4 KiB-aligned
+ * 16 MiB bounce buffers, one per thread.  `host` must be a valid mapping of
+ * the whole chunk.  Pure host code; the calls block until done and may run
+ * concurrently on distinct chunks.
  * ------------------------------------------------------------------------- */
 #define KVIO_DISK_PAGE_FIRST 0
 #define KVIO_DISK_LAYER_FIRST 1

@@ -2,7 +2,9 @@
 // whole-page transfers between a disk store and a pinned host chunk, as
 // parallel positioned reads / writes of merged contiguous pieces.
 #include <errno.h>
+#include <fcntl.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 #include <unistd.h>
 
@@ -76,27 +78,69 @@ kvio_status build(const kvio_disk_store *st, const int64_t *pages, int32_t n, in
     return KVIO_OK;
 }
 
+// Host memory the kernel cannot pin for direct I/O (the HIP runtime's pinned
+// allocations are device-file mappings) makes an O_DIRECT transfer fail with
+// EFAULT.  On O_DIRECT descriptors such transfers are staged through an
+// aligned bounce buffer per worker thread instead.
+constexpr size_t kBounceBytes = size_t(16) << 20;
+
+struct Bounce {
+    uint8_t *p = nullptr;
+    ~Bounce() { free(p); }
+    bool ready() { return p != nullptr || posix_memalign(reinterpret_cast<void **>(&p), 4096, kBounceBytes) == 0; }
+};
+
+// One transfer of up to len bytes between host + off and the file at file_off;
+// returns what pread/pwrite return.
+ssize_t transfer(int fd, uint8_t *host, int64_t len, int64_t file_off, bool to_host, Bounce *bounce) {
+    if (bounce == nullptr)
+        return to_host ? pread(fd, host, size_t(len), file_off) : pwrite(fd, host, size_t(len), file_off);
+    const size_t n = std::min<size_t>(size_t(len), kBounceBytes);
+    if (to_host) {
+        const ssize_t r = pread(fd, bounce->p, n, file_off);
+        if (r > 0) memcpy(host, bounce->p, size_t(r));
+        return r;
+    }
+    memcpy(bounce->p, host, n);
+    return pwrite(fd, bounce->p, n, file_off);
+}
+
 kvio_status run(int fd, const std::vector<Piece> &pieces, uint8_t *host, bool to_host, int32_t threads,
                 const char *fn, std::string *err) {
+    const int fl = fcntl(fd, F_GETFL);
+    if (fl < 0) {
+        *err = std::string(fn) + ": bad file descriptor";
+        return KVIO_EINVAL;
+    }
+    const bool direct = (fl & O_DIRECT) != 0;
     std::atomic<size_t> next{0};
     std::atomic<int> failed{0};
+    std::atomic<bool> staged{false};   // set once a direct transfer reported EFAULT
     std::mutex mu;
+    auto fail = [&](const std::string &why) {
+        std::lock_guard<std::mutex> g(mu);
+        if (!failed.exchange(1)) *err = std::string(fn) + ": " + why;
+    };
     auto worker = [&]() {
+        Bounce bounce;
         for (;;) {
             const size_t i = next.fetch_add(1);
             if (i >= pieces.size() || failed.load()) return;
             const Piece &pc = pieces[i];
             int64_t done = 0;
             while (done < pc.len) {
-                const ssize_t r = to_host ? pread(fd, host + pc.host_off + done, size_t(pc.len - done), pc.file_off + done)
-                                          : pwrite(fd, host + pc.host_off + done, size_t(pc.len - done), pc.file_off + done);
-                if (r < 0 && errno == EINTR) continue;
-                if (r <= 0) {
-                    std::lock_guard<std::mutex> g(mu);
-                    if (!failed.exchange(1))
-                        *err = std::string(fn) + (r < 0 ? std::string(": ") + strerror(errno) : ": short transfer at end of file");
-                    return;
+                Bounce *b = nullptr;
+                if (staged.load()) {
+                    if (!bounce.ready()) return fail("cannot allocate a bounce buffer");
+                    b = &bounce;
                 }
+                const ssize_t r = transfer(fd, host + pc.host_off + done, pc.len - done, pc.file_off + done, to_host, b);
+                if (r < 0 && errno == EINTR) continue;
+                if (r < 0 && errno == EFAULT && direct && b == nullptr) {
+                    staged.store(true);
+                    continue;
+                }
+                if (r <= 0) return fail(r < 0 ? std::string(strerror(errno)) : std::string("short transfer at end of file"));
                 done += r;
             }
         }
