@@ -69,6 +69,12 @@ def parse():
                     help="resource-quota sweep (Strata Fig. 5 analogue): load GB/s and the slowdown of a "
                          "co-running prefill-like GEMM and decode-like HBM-bound kernel vs. the load's "
                          "workgroup quota, on the Llama-3.1-8B page-size-1 workload")
+    ap.add_argument("--page-sweep", action="store_true",
+                    help="Llama-3.1-8B KV: kvio vs one hipMemcpyAsync per page segment over page sizes "
+                         "1..256 (32K tokens), plus 8192 tokens at page size 32")
+    ap.add_argument("--schedule", action="store_true",
+                    help="cache-aware batch formation: scheduling cost per round, and FIFO vs Algorithm 1 "
+                         "on a synthetic queue under a cost model built from measured load and GEMM rates")
     ap.add_argument("--disk", action="store_true",
                     help="storage tier: 8192 tokens at page size 32 from a local disk store into pinned "
                          "host memory, page-first vs layer-first, then into the paged pool")
@@ -700,6 +706,241 @@ def run_interference(args, torch, kv, W):
     print(json.dumps(res), flush=True)
 
 
+def run_page_sweep(args, torch, kv, W):
+    """GB/s against page size (the synthetic analogue of Fig. 10's page-size
+    axis) and the paper's own microbenchmark of Fig. 3 (8192 tokens at page
+    size 32), Llama-3.1-8B KV.  For every page size: kvio_load and
+    kvio_offload of the context (median of 5 after a warm-up, HIP events on
+    the transfer stream) and the naive path -- one hipMemcpyAsync per
+    (page, layer, K|V) segment of P*R bytes -- timed over at most 2^17 calls
+    (a prefix of the context's pages when there are more).  The pool holds
+    2^19 slots, so every page size divides it; pages are a random sample of
+    the pool's pages in random order."""
+    shp = W.LLAMA8B
+    L, H, D, R = shp.num_layers, shp.num_kv_heads, shp.head_dim, shp.row_bytes
+    S = 1 << 19
+    cases = [(32768, P) for P in (1, 2, 4, 16, 32, 64, 256)] + [(8192, 32)]
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    pool_t.view(torch.int16).fill_(0x5A5A)
+    Tmax = max(T for T, _ in cases)
+    nb_max = L * 2 * Tmax * R
+    host, out = kv.HostBuffer(nb_max), kv.HostBuffer(nb_max)
+    W.fill_cuda(host.ptr, nb_max, W.data_seed(2), shp)
+    stream = io_stream(torch, kv)
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    rows = []
+    try:
+        for T, P in cases:
+            rng = np.random.default_rng(500 + P + T)
+            pages = W.random_pages(rng, S // P, -(-T // P)) if P > 1 else W.random_slots(rng, S, T)
+            pidx = torch.from_numpy(pages).cuda()
+            nb = L * 2 * T * R
+            pool = kv.KVPool(pool_t, P)
+            span_in, span_out = [(host.ptr, T, T, pidx.data_ptr())], [(out.ptr, T, T, pidx.data_ptr())]
+            row = {"tokens": T, "page_size": P, "bytes": nb, "segment_bytes": P * R}
+            for name, fn in (("load", lambda: pool.load(span_in, stream=stream)),
+                             ("offload", lambda: pool.offload(span_out, stream=stream))):
+                fn()
+                torch.cuda.synchronize()
+                t = Timer(torch, stream)
+                for _ in range(5):
+                    e = t.start()
+                    fn()
+                    t.stop(e)
+                torch.cuda.synchronize()
+                ms = statistics.median(t.ms())
+                row[f"kvio_{name}_gbps"] = round(nb / (ms * 1e-3) / GB, 3)
+            pool.check()
+            if not np.array_equal(out.array[:nb], host.array[:nb]):
+                raise SystemExit(f"round trip differs at page size {P}")
+            max_calls = 1 << 17
+            n_pages = min(len(pages), max(1, max_calls // (L * 2)))
+            nt = min(T, n_pages * P)
+            kv.kvio_naive_load(pool.handle, [(host.ptr, T, min(nt, P * 4), pidx.data_ptr())], 0, 1, stream)
+            torch.cuda.synchronize()
+            t = Timer(torch, stream)
+            c0 = time.perf_counter()
+            e = t.start()
+            kv.kvio_naive_load(pool.handle, [(host.ptr, T, nt, pidx.data_ptr())], 0, L, stream)
+            t.stop(e)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - c0
+            nbn = L * 2 * nt * R
+            row["naive_calls"] = L * 2 * (-(-nt // P))
+            row["naive_prefix_of_calls"] = round(row["naive_calls"] / (L * 2 * (-(-T // P))), 4)
+            row["naive_load_gbps"] = round(nbn / max(wall, t.ms()[0] * 1e-3) / GB, 3)
+            row["speedup_vs_naive"] = round(row["kvio_load_gbps"] / row["naive_load_gbps"], 1)
+            if peak:
+                row["load_frac_of_h2d_peak"] = round(row["kvio_load_gbps"] / peak["h2d"], 4)
+            pool.close()
+            log(", ".join(f"{k2} {v}" for k2, v in row.items()))
+            rows.append(row)
+    finally:
+        host.free()
+        out.free()
+    res = base_result(args, min(r["kvio_load_gbps"] for r in rows), 0.0,
+                      "page-size sweep: Llama-3.1-8B KV, 32K tokens at page sizes 1..256 and 8192 tokens at "
+                      "page size 32, pool of 2^19 slots", {"pool_slots": S})
+    res["metric"] = "kvio vs per-page hipMemcpyAsync load GB/s against page size"
+    res["host_link_peak"] = {k2: round(v, 3) for k2, v in peak.items()} if peak else None
+    res["sweep"] = rows
+    print(json.dumps(res), flush=True)
+
+
+def synthetic_queue(n, seed, bursty=False):
+    """n requests (load_tokens, compute_tokens, context or None, 0): half reuse
+    a cached 8K-128K-token context (log-uniform) with 64-512 new tokens, a
+    third of those sharing the previous request's context (a bundle hit);
+    half are fresh 1K-8K-token prompts.  Shuffled: kinds drawn independently;
+    bursty: runs of 1-8 requests of one kind (sessions arriving together)."""
+    rng = np.random.default_rng(seed)
+    if bursty:
+        kinds = []
+        while len(kinds) < n:
+            kinds += [bool(rng.random() < 0.5)] * int(rng.integers(1, 9))
+        kinds = kinds[:n]
+    else:
+        kinds = [bool(x) for x in rng.random(n) < 0.5]
+    q, ctx = [], 0
+    for cached in kinds:
+        if cached:
+            if q and q[-1][2] is not None and rng.random() < 1 / 3:
+                q.append((q[-1][0], int(rng.integers(64, 512)), q[-1][2], 0))
+            else:
+                ctx += 1
+                q.append((int(np.exp(rng.uniform(np.log(8192), np.log(131072)))), int(rng.integers(64, 512)),
+                          ctx, 0))
+        else:
+            q.append((0, int(rng.integers(1024, 8192)), None, 0))
+    return q
+
+
+def drain_queue(kv, q, ratio, load_tok_s, prefill_tok_s, max_tokens=8192, max_requests=16):
+    """Schedule rounds until the queue is empty (every request present at
+    time 0); each batch costs max(load time, compute time) (layer-wise
+    overlap), a shared context loading once per batch.  Returns the drain
+    time, the mean completion time of a request, and batch counts."""
+    cur = list(range(len(q)))
+    total, batches, loading_bound = 0.0, 0, 0
+    done = []
+    while cur:
+        batch, rest = kv.kvio_schedule_round([q[i] for i in cur], max_tokens, max_requests, ratio)
+        loaded, load_tok, comp_tok = set(), 0, 0
+        for j in batch:
+            ld, cp, cx, _ = q[cur[j]]
+            if cx is None or cx not in loaded:
+                load_tok += ld
+            if cx is not None:
+                loaded.add(cx)
+            comp_tok += cp
+        t_load, t_comp = load_tok / load_tok_s, comp_tok / prefill_tok_s
+        total += max(t_load, t_comp)
+        done += [total] * len(batch)
+        loading_bound += t_load > t_comp
+        batches += 1
+        cur = [cur[j] for j in rest]
+    return {"drain_s": round(total, 4), "mean_completion_s": round(float(np.mean(done)), 4), "batches": batches,
+            "loading_bound_batches": loading_bound}
+
+
+def run_schedule(args, torch, kv, W):
+    """Cache-aware batch formation measured two ways.
+
+    (1) Host cost of kvio_schedule_round on queues of 64 .. 16,384 requests.
+    (2) FIFO (no loading-bound test) against Algorithm 1 draining the same
+    synthetic queue, with every batch timed by a cost model whose rates are
+    measured in this run: load time = cached tokens x 128 KiB / kvio_load GB/s
+    (Llama-3.1-8B KV, page size 16), compute time = new tokens / prefill
+    tokens/s, where prefill tokens/s = the measured bf16 GEMM rate / (2 x 8.03e9
+    FLOP per token, the 8B model's dense work).  Loads overlap compute layer
+    by layer, so a batch takes max(load, compute).  The queue mixes the
+    paper's two request kinds (see synthetic_queue), all present at time 0."""
+    shp = W.LLAMA8B
+    L, H, D, R = shp.num_layers, shp.num_kv_heads, shp.head_dim, shp.row_bytes
+    tok_bytes = L * 2 * R
+    # ---- measured rates ------------------------------------------------------------------
+    P, T, S = 16, 16384, 1 << 17
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    pidx = torch.from_numpy(W.random_pages(np.random.default_rng(600), S // P, T // P)).cuda()
+    stream = io_stream(torch, kv)
+    with kv.HostBuffer(T * tok_bytes) as hb:
+        hb.array[::4096] = 1
+        pool = kv.KVPool(pool_t, P)
+        span = [(hb.ptr, T, T, pidx.data_ptr())]
+        pool.load(span, stream=stream)
+        torch.cuda.synchronize()
+        t = Timer(torch, stream)
+        for _ in range(5):
+            e = t.start()
+            pool.load(span, stream=stream)
+            t.stop(e)
+        torch.cuda.synchronize()
+        pool.check()
+        pool.close()
+    load_gbps = T * tok_bytes / (statistics.median(t.ms()) * 1e-3) / GB
+    del pool_t
+    g = torch.Generator(device="cuda").manual_seed(8)
+    A = torch.randn(8192, 4096, device="cuda", dtype=torch.bfloat16, generator=g)
+    B = torch.randn(4096, 14336, device="cuda", dtype=torch.bfloat16, generator=g)
+    C = torch.empty(8192, 14336, device="cuda", dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(A, B, out=C)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(20):
+        torch.matmul(A, B, out=C)
+    b.record()
+    torch.cuda.synchronize()
+    gemm_tflops = 20 * 2 * 8192 * 4096 * 14336 / (a.elapsed_time(b) * 1e-3) / 1e12
+    del A, B, C
+    load_tok_s = load_gbps * GB / tok_bytes
+    prefill_tok_s = gemm_tflops * 1e12 / (2 * 8.03e9)
+    cost_ratio = load_tok_s / prefill_tok_s
+    log(f"kvio load {load_gbps:.2f} GB/s = {load_tok_s:.0f} tokens/s; bf16 GEMM {gemm_tflops:.0f} TFLOP/s = "
+        f"{prefill_tok_s:.0f} prefill tokens/s; loading-bound when load tokens > {cost_ratio:.2f} x compute tokens")
+
+    # ---- (1) host cost of one scheduling round ---------------------------------------------
+    cost = {}
+    for n in (64, 1024, 16384):
+        q = synthetic_queue(n, 700 + n)
+        kv.kvio_schedule_round(q, 8192, 16)
+        reps = 200 if n <= 1024 else 20
+        c0 = time.perf_counter()
+        for _ in range(reps):
+            kv.kvio_schedule_round(q, 8192, 16)
+        cost[n] = (time.perf_counter() - c0) / reps * 1e6
+    log("scheduling round (incl. ctypes marshalling): " + ", ".join(f"{n} requests {u:.1f} us"
+                                                                   for n, u in cost.items()))
+
+    # ---- (2) FIFO vs Algorithm 1 under the measured cost model -------------------------------
+    sim = {}
+    for order in ("shuffled", "bursty"):
+        q = synthetic_queue(512, 800, bursty=order == "bursty")
+        r = {"fifo": drain_queue(kv, q, float("inf"), load_tok_s, prefill_tok_s),
+             "algorithm1_ratio_100": drain_queue(kv, q, 100.0, load_tok_s, prefill_tok_s),
+             "algorithm1_ratio_cost_model": drain_queue(kv, q, cost_ratio, load_tok_s, prefill_tok_s)}
+        for k2 in ("algorithm1_ratio_100", "algorithm1_ratio_cost_model"):
+            r[k2]["drain_speedup_vs_fifo"] = round(r["fifo"]["drain_s"] / r[k2]["drain_s"], 3)
+            r[k2]["completion_speedup_vs_fifo"] = round(r["fifo"]["mean_completion_s"] / r[k2]["mean_completion_s"], 3)
+        r["aggregate_load_s"] = round(sum(x[0] for x in q) / load_tok_s, 3)
+        r["aggregate_compute_s"] = round(sum(x[1] for x in q) / prefill_tok_s, 3)
+        sim[order] = r
+        log(f"drain 512 requests ({order}): " + "; ".join(f"{k2} {v}" for k2, v in r.items()))
+    res = base_result(args, load_gbps, 0.0,
+                      "batch formation: 512 synthetic requests (half cached 8K-128K-token contexts with 64-512 new "
+                      "tokens, half fresh 1K-8K-token prompts; shuffled and bursty orders), token budget 8192, "
+                      "at most 16 requests per batch",
+                      {"kv_shape": shp.name, "page_size": P})
+    res["metric"] = "batch formation: queue drain time under measured load/compute rates, FIFO vs Algorithm 1"
+    res["rates"] = {"kvio_load_gbps": round(load_gbps, 3), "load_tokens_per_s": round(load_tok_s, 1),
+                    "gemm_tflops": round(gemm_tflops, 1), "prefill_tokens_per_s": round(prefill_tok_s, 1),
+                    "cost_model_ratio": round(cost_ratio, 3)}
+    res["schedule_round_us"] = {str(n): round(u, 2) for n, u in cost.items()}
+    res["simulation"] = sim
+    print(json.dumps(res), flush=True)
+
+
 def _open_store(path, direct):
     """O_DIRECT when the filesystem takes it; otherwise a buffered descriptor
     whose cached pages are dropped before every timed read."""
@@ -719,15 +960,15 @@ def run_disk(args, torch, kv, W):
     descriptors (pinned chunks are then staged through bounce buffers) and
     through buffered ones with the file's cached pages dropped before every
     read.  The context's 256
-    pages sit at random disk pages of a 320-page store, so no two reads merge
-    by accident.  Both stores hold the same logical KV; after timing, the
+    pages sit at random disk pages of a 1024-page store (other contexts fill
+    the rest), so reads rarely merge and read-ahead rarely helps by accident.  Both stores hold the same logical KV; after timing, the
     layer-first store is also read into a page-first chunk (pieces of P*R) and
     must equal the page-first result, and the two chunks loaded into the
     layer-first paged pool (kvio_load, host layout to match) must give equal
     pools."""
     P, T = 32, 8192
     n_ctx = T // P
-    N = n_ctx + n_ctx // 4
+    N = 4 * n_ctx
     threads = [int(x) for x in args.disk_threads.split(",")]
     reps = 3
     rows = []
@@ -861,6 +1102,10 @@ def main():
             run_interference(args, torch, kv, W)
         elif args.disk:
             run_disk(args, torch, kv, W)
+        elif args.page_sweep:
+            run_page_sweep(args, torch, kv, W)
+        elif args.schedule:
+            run_schedule(args, torch, kv, W)
         elif k in EXTRA_MODES:
             EXTRA_MODES[k](args, torch, kv, W)
         else:
