@@ -180,12 +180,16 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
             t.stop(e)
         torch.cuda.synchronize()
         res[name] = nbytes / (statistics.median(t.ms()) * 1e-3) / GB
-    # bidirectional: H2D of one half while D2H of the other half.  The runtime
-    # binds each stream to a copy engine on its own; two streams can land on
-    # one engine and serialise, so several stream pairs are tried and the best
-    # (the link's real bidirectional capacity) is kept.
+    # bidirectional: H2D of one half while D2H of the other half.  Copies on
+    # two ordinary streams can serialise (they may share a hardware queue);
+    # pairs that include the transfer stream (a queue of its own) or the null
+    # stream run concurrently, but not reliably on every run, so several such
+    # pairs are tried and the best (the link's real bidirectional capacity)
+    # is kept.
     best = 0.0
-    pairs = [(s1, s2), (s2, torch.cuda.Stream()), (torch.cuda.Stream(), torch.cuda.Stream())]
+    null = torch.cuda.default_stream()
+    pairs = [(s1, s2)] + [(s1, torch.cuda.Stream()) for _ in range(3)] + \
+            [(null, torch.cuda.Stream()) for _ in range(3)] + [(torch.cuda.Stream(), null)]
     for a, b in pairs:
         ts = []
         for _ in range(reps):
