@@ -255,6 +255,30 @@ kvio_status kvio_disk_store_pages(const kvio_disk_store *store, const int64_t *d
                                   const void *host, int64_t host_tokens, int32_t host_layout,
                                   int32_t threads);
 
+/* Background prefetch (Sec. 4.2.1): a storage hit starts the prefetch while
+ * the request waits in the queue; at dispatch the controller stops whatever is
+ * still in flight and uses the pages that already reached host memory.
+ *
+ * kvio_disk_prefetch_start validates like kvio_disk_prefetch, then returns at
+ * once with `threads` worker threads reading in the background; *out is the
+ * job handle (NULL on error).  The store's descriptor and the host chunk must
+ * stay valid until kvio_disk_prefetch_finish returns.
+ * kvio_disk_prefetch_progress: pages complete so far (never blocks).
+ * kvio_disk_prefetch_finish: with cancel != 0 the workers stop at their next
+ * transfer boundary (at most one piece or one bounce buffer each); then it
+ * waits for them, writes page_done[j] = 1 for every context page j whose bytes
+ * have all arrived and 0 otherwise (page_done may be NULL; it holds n_pages
+ * bytes), stores the count in *pages_done (may be NULL), and frees the job.
+ * Bytes of incomplete pages are unspecified.  Returns KVIO_EIO if a read
+ * failed (page_done still names the complete pages), else KVIO_OK -- also
+ * after a cancellation.  Every job must be finished exactly once. */
+typedef struct kvio_prefetch *kvio_prefetch_t;
+kvio_status kvio_disk_prefetch_start(const kvio_disk_store *store, const int64_t *disk_pages, int32_t n_pages,
+                                     void *host, int64_t host_tokens, int32_t host_layout, int32_t threads,
+                                     kvio_prefetch_t *out);
+kvio_status kvio_disk_prefetch_progress(kvio_prefetch_t job, int32_t *pages_done);
+kvio_status kvio_disk_prefetch_finish(kvio_prefetch_t job, int32_t cancel, uint8_t *page_done, int32_t *pages_done);
+
 /* ---------------------------------------------------------------------------
  * Cache-aware batch formation (Sec. 4.3): the host-side step that decides
  * which queued prefill requests the next batch loads and computes.

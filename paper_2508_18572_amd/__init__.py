@@ -12,6 +12,6 @@ from .kvio import (  # noqa: F401
     kvio_check, kvio_host_alloc, kvio_host_free, kvio_last_error, kvio_load, kvio_load_layer,
     kvio_memcpy, kvio_naive_load, kvio_naive_offload, kvio_offload, kvio_pool_create,
     kvio_pool_destroy, kvio_span, kvio_strerror, launch, make_spans, Stream,
-    kvio_stream_create, kvio_stream_destroy, kvio_schedule_round, kvio_disk_prefetch, kvio_disk_store_pages,
+    kvio_stream_create, kvio_stream_destroy, kvio_schedule_round, kvio_disk_prefetch, kvio_disk_store_pages, DiskPrefetch,
     KVIO_DISK_PAGE_FIRST, KVIO_DISK_LAYER_FIRST, KVIO_EIO,
 )

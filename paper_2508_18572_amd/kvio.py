@@ -17,6 +17,7 @@ import ctypes
 import os
 from typing import Iterable, Optional, Sequence, Tuple, Union
 
+import numpy as np
 import torch  # noqa: F401  (binds the HIP runtime before libkvio.so loads)
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -108,6 +109,10 @@ def _load_library() -> ctypes.CDLL:
         "kvio_stream_destroy": [vp],
         "kvio_disk_prefetch": [ctypes.POINTER(kvio_disk_store), ctypes.POINTER(i64), i32, vp, i64, i32, i32],
         "kvio_disk_store_pages": [ctypes.POINTER(kvio_disk_store), ctypes.POINTER(i64), i32, vp, i64, i32, i32],
+        "kvio_disk_prefetch_start": [ctypes.POINTER(kvio_disk_store), ctypes.POINTER(i64), i32, vp, i64, i32, i32,
+                                     ctypes.POINTER(vp)],
+        "kvio_disk_prefetch_progress": [vp, ctypes.POINTER(i32)],
+        "kvio_disk_prefetch_finish": [vp, i32, ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(i32)],
         "kvio_schedule_round": [ctypes.POINTER(kvio_request), i32, ctypes.POINTER(kvio_batch_policy),
                                 ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32),
                                 ctypes.POINTER(i32)],
@@ -129,7 +134,8 @@ _lib = _load_library()
 EXPORTS = ("kvio_pool_create", "kvio_pool_destroy", "kvio_load", "kvio_offload", "kvio_load_layer",
            "kvio_check", "kvio_naive_load", "kvio_naive_offload", "kvio_memcpy", "kvio_host_alloc",
            "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_schedule_round",
-           "kvio_disk_prefetch", "kvio_disk_store_pages",
+           "kvio_disk_prefetch", "kvio_disk_store_pages", "kvio_disk_prefetch_start", "kvio_disk_prefetch_progress",
+           "kvio_disk_prefetch_finish",
            "kvio_strerror", "kvio_last_error")
 
 
@@ -326,11 +332,53 @@ def kvio_disk_store_pages(fd: int, disk_layout: int, num_disk_pages: int, num_la
                                       host_layout, threads))
 
 
+class DiskPrefetch:
+    """A background prefetch of a context's disk pages into a host chunk
+    (kvio_disk_prefetch_start); finish() stops it (cancel=True) or waits for
+    it, and returns which context pages arrived in full."""
+
+    def __init__(self, fd: int, disk_layout: int, num_disk_pages: int, num_layers: int, page_size: int,
+                 row_bytes: int, disk_pages, host_ptr: int, host_tokens: int,
+                 host_layout: int = KVIO_HOST_TOKEN_MAJOR, threads: int = 8):
+        self._st, self._pages = _disk_args(fd, disk_layout, num_disk_pages, num_layers, page_size, row_bytes,
+                                           disk_pages)
+        self.n_pages = len(disk_pages)
+        h = ctypes.c_void_p()
+        _check(_lib.kvio_disk_prefetch_start(ctypes.byref(self._st), self._pages, self.n_pages, host_ptr,
+                                             host_tokens, host_layout, threads, ctypes.byref(h)))
+        self._h = h
+
+    def progress(self) -> int:
+        n = ctypes.c_int32()
+        _check(_lib.kvio_disk_prefetch_progress(self._h, ctypes.byref(n)))
+        return n.value
+
+    def finish(self, cancel: bool = False) -> np.ndarray:
+        """Bool array: page j arrived in full.  A failed read raises KvioError
+        whose `page_done` attribute holds the same array."""
+        if self._h is None:
+            raise RuntimeError("prefetch already finished")
+        done = (ctypes.c_uint8 * max(self.n_pages, 1))()
+        n = ctypes.c_int32()
+        st = _lib.kvio_disk_prefetch_finish(self._h, 1 if cancel else 0, done, ctypes.byref(n))
+        self._h = None
+        page_done = np.frombuffer(bytes(done), np.uint8)[:self.n_pages].astype(bool)
+        if st != KVIO_OK:
+            err = KvioError(st, kvio_last_error())
+            err.page_done = page_done
+            raise err
+        assert int(page_done.sum()) == n.value
+        return page_done
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and _lib is not None:
+            _lib.kvio_disk_prefetch_finish(self._h, 1, None, None)
+
+
 class HostBuffer:
     """Pinned, device-mapped host memory from kvio_host_alloc, with a numpy view."""
 
     def __init__(self, nbytes: int, flags: int = KVIO_HOST_COHERENT):
-        import numpy as np
         self.nbytes = nbytes
         self.ptr = kvio_host_alloc(nbytes, flags)
         self.array = np.ctypeslib.as_array((ctypes.c_uint8 * nbytes).from_address(self.ptr))
