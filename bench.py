@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--host-layout", choices=["token", "page", "head"], default="token",
                     help="host chunk layout: token-major (default), page-first, or head-major")
     ap.add_argument("--no-lds", action="store_true", help="head-major chunks: direct gather, no LDS staging")
+    ap.add_argument("--staged", action="store_true",
+                    help="copy engine through an HBM staging buffer + scatter/gather kernel (KVIO_LAUNCH_STAGED)")
+    ap.add_argument("--staging-mib", type=int, default=0, help="staging per direction (4 slots); 0 = default")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-peak", action="store_true")
@@ -292,7 +295,8 @@ def h2d_d2h_peak(torch, kv, nbytes=2 << 30):
 
 
 def launch_from(args, kv):
-    flags = (kv.KVIO_LAUNCH_CACHED if args.cached else 0) | (kv.KVIO_LAUNCH_NO_LDS if args.no_lds else 0)
+    flags = (kv.KVIO_LAUNCH_CACHED if args.cached else 0) | (kv.KVIO_LAUNCH_NO_LDS if args.no_lds else 0) | \
+        (kv.KVIO_LAUNCH_STAGED if args.staged else 0)
     return kv.launch(args.workgroups, args.threads, args.tile_kib, flags)
 
 
@@ -319,7 +323,8 @@ def run_layerwise(args, torch, kv, W):
     host = kv.HostBuffer(nbytes)
     peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
     W.fill_cuda(host.ptr, nbytes, W.data_seed(k), shp)
-    pool = kv.KVPool(pool_t, P, load_launch=launch_from(args, kv), host_layout=layout_from(args, kv))
+    pool = kv.KVPool(pool_t, P, load_launch=launch_from(args, kv), host_layout=layout_from(args, kv),
+                     staging_bytes=args.staging_mib << 20)
     span = [(host.ptr, T, T, pidx.data_ptr())]
     side, comp = io_stream(torch, kv), torch.cuda.Stream()
     M, N, K = 4096, 8192, 8192
@@ -443,7 +448,7 @@ def run_batched(args, torch, kv, W):
         f"mean page-run length {req.mean_run_length:.2f}")
     pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
     lc = launch_from(args, kv)
-    pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc)
+    pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc, staging_bytes=args.staging_mib << 20)
     pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
     host = kv.HostBuffer(max(sum(sizes[i] for i in w) for w in waves))
     peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
@@ -516,7 +521,7 @@ def run_bidirectional(args, torch, kv, W):
     nb, nbo = L * 2 * T * R, L * 2 * TO * R
     pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
     lc = launch_from(args, kv)
-    pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc)
+    pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc, staging_bytes=args.staging_mib << 20)
     bg = [int(x) for x in args.bg_offload.split(",")]
     # a second handle on the same pool whose offloads run with the background quota
     pool_bg = kv.KVPool(pool_t, P, offload_launch=kv.launch(bg[0], bg[1], bg[2], 0))
@@ -665,13 +670,18 @@ def run_interference(args, torch, kv, W):
         return a.elapsed_time(b)
 
     quotas = [(1, 1024), (2, 1024), (4, 1024), (2, 256), (4, 256), (8, 256), (16, 256), (32, 256),
-              (64, 256), (128, 256), (32, 64), (64, 64), (128, 64), (256, 64), (64, 128), (128, 128)]
+              (64, 256), (128, 256), (32, 64), (64, 64), (128, 64), (256, 64), (64, 128), (128, 128),
+              ("staged", None)]
     rows = []
     base = {name: alone(fn) for name, fn in corunners.items()}
     log(f"co-runners alone: " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
     for wg, th in quotas:
-        pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
-        row = {"workgroups": wg, "threads": th, "waves": wg * th // 64,
+        if wg == "staged":     # copy engine + HBM scatter at the default scatter shape
+            pool = kv.KVPool(pool_t, P, load_launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED),
+                             staging_bytes=args.staging_mib << 20)
+        else:
+            pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
+        row = {"workgroups": wg, "threads": th, "waves": wg * th // 64 if th else None,
                "load_gbps_alone": round(nb / (load_alone(pool) * 1e-3) / GB, 3)}
         for name, fn in corunners.items():
             n_iter = int(200 / base[name]) + 20            # enough to outlast the load
@@ -699,7 +709,7 @@ def run_interference(args, torch, kv, W):
             row[f"{name}_slowdown"] = round(statistics.median(inside) / base[name], 4) if inside else None
         pool.close()
         rows.append(row)
-        log(f"quota {wg:3d} x {th:4d}: " + ", ".join(f"{k2} {v}" for k2, v in row.items()
+        log(f"quota {wg!s:>6} x {th!s:>4}: " + ", ".join(f"{k2} {v}" for k2, v in row.items()
                                                     if k2 not in ("workgroups", "threads")))
     res = base_result(args, max(r["load_gbps_alone"] for r in rows), 0.0,
                       "interference sweep on config2: Llama-3.1-8B KV, page size 1, 32K-token load",
@@ -1102,6 +1112,9 @@ def main():
         return
     k = args.config
     try:
+        # the transfer stream first: streams created later (the pool's own
+        # copy streams among them) then take the remaining hardware queues
+        io_stream(torch, kv)
         if args.interference:
             run_interference(args, torch, kv, W)
         elif args.disk:
@@ -1145,7 +1158,8 @@ def run_single(args, torch, kv, W, k):
     log(f"host chunk {host_bytes / 2**30:.2f} GiB filled in {time.perf_counter() - t0:.1f}s")
 
     launch = launch_from(args, kv)
-    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch, host_layout=layout_from(args, kv))
+    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch, host_layout=layout_from(args, kv),
+                     staging_bytes=args.staging_mib << 20)
     span_in = [(host.ptr, T, T, pidx.data_ptr())]
     span_out = [(out.ptr, T, T, pidx.data_ptr())]
     stream = io_stream(torch, kv)
@@ -1225,7 +1239,7 @@ def run_single(args, torch, kv, W, k):
             f"{steady['single_shot_us']:.1f} us; same-size memcpy {steady['memcpy_gbps']:.2f} GB/s")
 
     default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host
-                          or args.no_lds or args.host_layout != "token")
+                          or args.no_lds or args.staged or args.host_layout != "token")
     traffic = measured_traffic(k, default_launch)
     frac_h2d = load_gbps / peak["h2d"] if peak else None
     frac_d2h = off_gbps / peak["d2h"] if peak else None
@@ -1248,7 +1262,8 @@ def run_single(args, torch, kv, W, k):
                    "tokens": T, "payload_bytes_per_direction": payload,
                    "step": "kvio_load (all layers) + kvio_offload (all layers)",
                    "launch": {"workgroups": args.workgroups or "default", "threads": args.threads or "default",
-                              "tile_kib": args.tile_kib or "default", "nontemporal": not args.cached},
+                              "tile_kib": args.tile_kib or "default", "nontemporal": not args.cached,
+                              "staged": args.staged},
                    "host_memory": "non-coherent" if args.noncoherent_host else "coherent",
                    "host_layout": args.host_layout + ("" if not args.no_lds else " (no LDS)"),
                    "io_stream": _IO.get("kind")},

@@ -96,6 +96,26 @@ typedef enum kvio_status {
  * take the library defaults.  Results never depend on these. */
 #define KVIO_LAUNCH_CACHED 0x1     /* plain loads/stores instead of non-temporal ones */
 #define KVIO_LAUNCH_NO_LDS 0x2     /* head-major chunks: gather directly, no LDS staging */
+/* KVIO_LAUNCH_STAGED (token-major chunks only): instead of wavefronts reading
+ * (writing) the pinned chunk across the host link, the copy engine moves the
+ * chunk's contiguous (layer, K|V) token runs to (from) an HBM staging buffer
+ * of the pool handle with hipMemcpyAsync, and a kernel scatters (gathers) the
+ * rows between the staging buffer and the paged pool -- the layout conversion
+ * then runs at HBM speed on the whole chip for short bursts, and the long
+ * host-link phase occupies no compute unit.  The staging buffer is split into
+ * 4 slots: the copies run on the call's stream while the kernels run on a
+ * side stream the pool handle owns for that direction, each slot handed
+ * between them by events, so the copy engine never waits for a kernel that
+ * is queued behind other work.  The call keeps stream order: it starts after
+ * the work already on the call's stream, and the call's stream has passed
+ * all of its work (a load: its last scatter) when the call completes in
+ * stream order.  The launch fields shape the scatter / gather kernel (defaults
+ * 1024 x 256, 16 KiB steps).  Calls in one direction on one handle share that
+ * direction's staging, so they must not overlap (same stream, or ordered by
+ * events).  An out-of-range page is still skipped and reported by kvio_check,
+ * but a staged offload then leaves unspecified bytes in the host rows of its
+ * tokens. */
+#define KVIO_LAUNCH_STAGED 0x4
 typedef struct kvio_launch {
     int32_t workgroups;   /* workgroups per launch, >= 1; 0 = default                       */
     int32_t threads;      /* threads per workgroup: multiple of 64 in [64, 1024]; 0 = default */
@@ -116,6 +136,10 @@ typedef struct kvio_pool_desc {
     void *const *v_layers;    /* host array of L device pointers, each S * R bytes       */
     kvio_launch load_launch;  /* launch shape of load kernels                            */
     kvio_launch offload_launch; /* launch shape of offload kernels                       */
+    int64_t staging_bytes;    /* HBM staging per direction with KVIO_LAUNCH_STAGED: 4 slots
+                                 of staging_bytes / 4 (rounded down to 16 B), each >= 2 * P
+                                 * R; 0 = 1 GiB.  Allocated by kvio_pool_create, with a
+                                 side stream and events, only for staged directions.      */
 } kvio_pool_desc;
 
 typedef struct kvio_pool *kvio_pool_t;
@@ -139,8 +163,9 @@ typedef struct kvio_span {
  * KVIO_EHIP).  *out is set only on success. */
 kvio_status kvio_pool_create(const kvio_pool_desc *desc, kvio_pool_t *out);
 
-/* Free the handle.  The caller must have synchronised every stream that still
- * runs a transfer on it.  NULL is accepted. */
+/* Free the handle (waiting for its own side streams first).  The caller must
+ * have synchronised every stream that still runs a transfer on it.  NULL is
+ * accepted. */
 kvio_status kvio_pool_destroy(kvio_pool_t pool);
 
 /* Load (Sec. 4.2): move tokens [0, num_tokens) of each of the n_spans contexts,

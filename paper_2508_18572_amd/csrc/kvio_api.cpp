@@ -49,6 +49,14 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 constexpr int kDefaultThreads = 256;
 constexpr kvio::Shape kDefaultLoad = {16, kDefaultThreads, 4, true, true};
 constexpr kvio::Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
+// Staged transfers: the scatter / gather between the HBM staging buffer and
+// the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at
+// page size 1 in 1.75 ms, 2.4 TB/s of payload).
+constexpr kvio::Shape kDefaultStaged = {1024, kDefaultThreads, 16, true, true};
+constexpr int64_t kDefaultStagingBytes = int64_t(1) << 30;
+// The staging buffer is split into this many slots so the copy engine fills
+// (drains) one while the kernel scatters (gathers) another.
+constexpr int kStageSlots = 4;
 
 kvio::Shape resolve(const kvio_launch &l, const kvio::Shape &def) {
     kvio::Shape s;
@@ -67,7 +75,7 @@ kvio_status check_launch(const kvio_launch &l, const char *which) {
         return fail(KVIO_EINVAL, "%s: threads %d is not a multiple of 64 in [64, 1024]", which, l.threads);
     if (l.tile_kib != 0 && l.tile_kib != 4 && l.tile_kib != 8 && l.tile_kib != 16)
         return fail(KVIO_EINVAL, "%s: tile_kib %d is not 4, 8 or 16", which, l.tile_kib);
-    if ((l.flags & ~(KVIO_LAUNCH_CACHED | KVIO_LAUNCH_NO_LDS)) != 0)
+    if ((l.flags & ~(KVIO_LAUNCH_CACHED | KVIO_LAUNCH_NO_LDS | KVIO_LAUNCH_STAGED)) != 0)
         return fail(KVIO_EINVAL, "%s: unknown launch flags 0x%x", which, l.flags);
     return KVIO_OK;
 }
@@ -140,7 +148,58 @@ struct kvio_pool {
     unsigned long long *d_err;       // device error record
     kvio_launch load_launch;
     kvio_launch offload_launch;
+    // KVIO_LAUNCH_STAGED, per direction: HBM staging split into kStageSlots
+    // slots, a side stream for the scatter / gather kernels, and the events
+    // that hand slots between it and the caller's stream.
+    uint8_t *stage[2];
+    int64_t slot_bytes;
+    hipStream_t side_stream[2];
+    hipEvent_t ev_filled[2][kStageSlots];
+    hipEvent_t ev_free[2][kStageSlots];
+    hipEvent_t ev_start[2];
+    hipEvent_t ev_done[2];
 };
+
+namespace {
+
+// Release what kvio_pool_create allocated (null members are skipped); waits
+// for the side streams first.  Returns the first failure.
+hipError_t release_pool(kvio_pool *p) {
+    hipError_t first = hipSuccess;
+    auto keep = [&](hipError_t e) { if (first == hipSuccess && e != hipSuccess) first = e; };
+    for (int dir = 0; dir < 2; ++dir) {
+        if (p->side_stream[dir] != nullptr) {
+            keep(hipStreamSynchronize(p->side_stream[dir]));
+            keep(hipStreamDestroy(p->side_stream[dir]));
+        }
+        for (int k = 0; k < kStageSlots; ++k) {
+            if (p->ev_filled[dir][k] != nullptr) keep(hipEventDestroy(p->ev_filled[dir][k]));
+            if (p->ev_free[dir][k] != nullptr) keep(hipEventDestroy(p->ev_free[dir][k]));
+        }
+        if (p->ev_start[dir] != nullptr) keep(hipEventDestroy(p->ev_start[dir]));
+        if (p->ev_done[dir] != nullptr) keep(hipEventDestroy(p->ev_done[dir]));
+        if (p->stage[dir] != nullptr) keep(hipFree(p->stage[dir]));
+    }
+    if (p->d_layers != nullptr) keep(hipFree(p->d_layers));
+    if (p->d_err != nullptr) keep(hipFree(p->d_err));
+    delete p;
+    return first;
+}
+
+// Staging buffer, side stream and events of one staged direction.
+hipError_t create_staging(kvio_pool *p, int dir, int64_t stage_bytes) {
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&p->stage[dir]), size_t(stage_bytes));
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->side_stream[dir], hipStreamNonBlocking);
+    for (int k = 0; k < kStageSlots && e == hipSuccess; ++k) {
+        e = hipEventCreateWithFlags(&p->ev_filled[dir][k], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->ev_free[dir][k], hipEventDisableTiming);
+    }
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&p->ev_start[dir], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&p->ev_done[dir], hipEventDisableTiming);
+    return e;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -186,6 +245,16 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
     if (st != KVIO_OK) return st;
     st = check_launch(d->offload_launch, "offload_launch");
     if (st != KVIO_OK) return st;
+    const bool staged[2] = {(d->load_launch.flags & KVIO_LAUNCH_STAGED) != 0,
+                            (d->offload_launch.flags & KVIO_LAUNCH_STAGED) != 0};
+    const int64_t stage_bytes = d->staging_bytes > 0 ? d->staging_bytes : kDefaultStagingBytes;
+    if ((staged[0] || staged[1]) && d->host_layout != KVIO_HOST_TOKEN_MAJOR)
+        return fail(KVIO_EINVAL, "kvio_pool_create: staged transfers take token-major host chunks");
+    const int64_t slot_bytes = stage_bytes / kStageSlots / 16 * 16;
+    if ((staged[0] || staged[1]) && (d->staging_bytes < 0 || slot_bytes < 2 * int64_t(d->page_size) * R))
+        return fail(KVIO_EINVAL, "kvio_pool_create: staging_bytes %lld must hold %d slots of at least one page "
+                    "of K and V rows (%lld bytes each)", (long long)d->staging_bytes, kStageSlots,
+                    (long long)(2 * int64_t(d->page_size) * R));
 
     kvio_pool *p = new (std::nothrow) kvio_pool();
     if (p == nullptr) return fail(KVIO_ENOMEM, "kvio_pool_create: host allocation failed");
@@ -201,6 +270,7 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
     p->layers.resize(2 * size_t(d->num_layers));
     p->d_layers = nullptr;
     p->d_err = nullptr;
+    p->slot_bytes = slot_bytes;
     const uint64_t layer_bytes = uint64_t(d->num_slots) * uint64_t(R);
     for (int kv = 0; kv < 2; ++kv) {
         void *const *tab = kv == 0 ? d->k_layers : d->v_layers;
@@ -234,10 +304,10 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
         e = hipMemcpy(p->d_layers, p->layers.data(), p->layers.size() * sizeof(uint8_t *),
                       hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(p->d_err, 0, sizeof(unsigned long long));
+    for (int dir = 0; dir < 2 && e == hipSuccess; ++dir)
+        if (staged[dir]) e = create_staging(p, dir, int64_t(kStageSlots) * slot_bytes);
     if (e != hipSuccess) {
-        (void)hipFree(p->d_layers);
-        (void)hipFree(p->d_err);
-        delete p;
+        (void)release_pool(p);
         return e == hipErrorOutOfMemory ? fail(KVIO_ENOMEM, "kvio_pool_create: device allocation failed")
                                         : fail_hip(e, "kvio_pool_create");
     }
@@ -248,11 +318,8 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
 kvio_status kvio_pool_destroy(kvio_pool_t p) {
     g_last_error.clear();
     if (p == nullptr) return KVIO_OK;
-    hipError_t e1 = hipFree(p->d_layers);
-    hipError_t e2 = hipFree(p->d_err);
-    delete p;
-    if (e1 != hipSuccess) return fail_hip(e1, "kvio_pool_destroy");
-    if (e2 != hipSuccess) return fail_hip(e2, "kvio_pool_destroy");
+    const hipError_t e = release_pool(p);
+    if (e != hipSuccess) return fail_hip(e, "kvio_pool_destroy");
     return KVIO_OK;
 }
 
@@ -325,6 +392,155 @@ kvio_status validate(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
     return KVIO_OK;
 }
 
+// Fields of a launch that do not depend on its spans.
+void common_args(kvio_pool_t p, const kvio::Shape &shape, int32_t l0, kvio::CopyArgs *a) {
+    memset(a, 0, sizeof *a);
+    const int64_t R = p->row_bytes;
+    a->layers = p->d_layers;
+    a->err = p->d_err;
+    a->row_bytes = R;
+    a->num_pages = p->num_slots / p->page_size;
+    a->num_layers = p->num_layers;
+    a->layer_begin = l0;
+    a->page_size = p->page_size;
+    a->page_shift = ilog2_exact(p->page_size);
+    a->vec_per_row = static_cast<int32_t>(R / 16);
+    a->vec_shift = ilog2_exact(R / 16);
+    a->rows_per_tile = kvio::rows_per_tile(R, shape.tile_kib);
+    a->host_layout = p->host_layout;
+    a->num_heads = p->num_heads;
+    a->seg_vecs = static_cast<int32_t>(p->seg_bytes / 16);
+}
+
+hipError_t launch_capped(const kvio::CopyArgs &a, kvio::Direction dir, kvio::Shape s, hipStream_t stream) {
+    const int64_t waves_per_wg = s.threads / 64;
+    const int64_t max_wgs = (a.total_tiles + waves_per_wg - 1) / waves_per_wg;
+    if (s.workgroups > max_wgs) s.workgroups = static_cast<int>(max_wgs);
+    return kvio::launch_copy(a, dir, s, stream);
+}
+
+// Staged transfer (KVIO_LAUNCH_STAGED).  Layer by layer, the spans' token
+// runs are packed into staging slots as units of n tokens: K rows
+// [t0, t0 + n) then V rows; a unit is as many tokens as fit (a multiple of P
+// unless it ends the span).  The copy engine works on the caller's stream,
+// the scatter / gather kernel on the pool's kernel stream for this
+// direction; events hand each slot over:
+//   load:    caller: [wait slot free] copies in -> filled
+//            kernel: wait filled -> scatter -> slot free
+//   offload: kernel: [wait slot free] gather -> filled
+//            caller: wait filled -> copies out -> slot free
+// An offload's kernel stream first waits for the work already on the
+// caller's stream (the pool rows it reads may come from it); a load ends
+// with the caller's stream waiting for the last scatter.  So the call keeps
+// stream order.  The kernel sees each unit as a one-layer span whose chunk
+// starts l*2*n*R bytes before the unit, so its usual row address
+// ((l*2 + kv)*n + t)*R lands inside the unit.
+kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvio_span *spans, int32_t n,
+                       int32_t l0, int32_t l1, hipStream_t stream, kvio::Direction dir, const kvio::Shape &shape,
+                       const char *fn) {
+    const int64_t R = p->row_bytes, P = p->page_size, cap = p->slot_bytes;
+    if (p->stage[dir] == nullptr) return fail(KVIO_EINVAL, "%s: the pool has no staging buffer for this direction", fn);
+    hipStream_t ks = p->side_stream[dir];
+    struct Unit { int32_t span; int64_t t0, n, off; };
+    std::vector<Unit> units;
+    units.reserve(KVIO_MAX_SPANS_PER_LAUNCH);
+    int64_t used = 0, chunk = 0;
+    hipError_t e = hipSuccess;
+    if (dir == kvio::kOffload) {
+        e = hipEventRecord(p->ev_start[dir], stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(ks, p->ev_start[dir], 0);
+        if (e != hipSuccess) return fail_hip(e, fn);
+    }
+    auto copy_unit = [&](const Unit &u, uint8_t *slot, int32_t l, bool to_stage) -> hipError_t {
+        uint8_t *host = static_cast<uint8_t *>(spans[u.span].host);
+        const int64_t ht = spans[u.span].host_tokens;
+        for (int kv = 0; kv < 2; ++kv) {
+            uint8_t *h = host + ((int64_t(l) * 2 + kv) * ht + u.t0) * R;
+            uint8_t *d = slot + u.off + kv * u.n * R;
+            hipError_t err = to_stage ? hipMemcpyAsync(d, h, size_t(u.n * R), hipMemcpyHostToDevice, stream)
+                                      : hipMemcpyAsync(h, d, size_t(u.n * R), hipMemcpyDeviceToHost, stream);
+            if (err != hipSuccess) return err;
+        }
+        return hipSuccess;
+    };
+    auto flush = [&](int32_t l) -> kvio_status {
+        if (units.empty()) return KVIO_OK;
+        const int k = int(chunk % kStageSlots);
+        uint8_t *slot = p->stage[dir] + int64_t(k) * cap;
+        hipEvent_t filled = p->ev_filled[dir][k], freed = p->ev_free[dir][k];
+        hipError_t err = hipSuccess;
+        if (dir == kvio::kLoad) {
+            if (chunk >= kStageSlots) err = hipStreamWaitEvent(stream, freed, 0);
+            for (size_t i = 0; i < units.size() && err == hipSuccess; ++i) err = copy_unit(units[i], slot, l, true);
+            if (err == hipSuccess) err = hipEventRecord(filled, stream);
+            if (err == hipSuccess) err = hipStreamWaitEvent(ks, filled, 0);
+        } else if (chunk >= kStageSlots) {
+            err = hipStreamWaitEvent(ks, freed, 0);
+        }
+        if (err != hipSuccess) return fail_hip(err, fn);
+        kvio::CopyArgs a;
+        common_args(p, shape, l, &a);
+        a.n_spans = static_cast<int32_t>(units.size());
+        int64_t tiles = 0;
+        for (size_t i = 0; i < units.size(); ++i) {
+            const Unit &u = units[i];
+            a.tile_prefix[i] = tiles;
+            a.spans[i].host = reinterpret_cast<const uint8_t *>(reinterpret_cast<uintptr_t>(slot) + uintptr_t(u.off) -
+                                                                uintptr_t(int64_t(l) * 2 * u.n * R));
+            a.spans[i].page_idx = rs[size_t(u.span)].page_idx + u.t0 / P;
+            a.spans[i].host_tokens = u.n;
+            a.spans[i].num_tokens = static_cast<int32_t>(u.n);
+            a.spans[i].origin = u.span;
+            a.spans[i].page_base = static_cast<int32_t>(u.t0 / P);
+            tiles += (u.n + a.rows_per_tile - 1) / a.rows_per_tile;
+        }
+        a.tile_prefix[units.size()] = tiles;
+        a.plane_tiles = tiles;
+        a.total_tiles = tiles * 2;
+        if ((err = launch_capped(a, dir, shape, ks)) != hipSuccess) return fail_hip(err, fn);
+        if (dir == kvio::kLoad) {
+            err = hipEventRecord(freed, ks);
+        } else {
+            err = hipEventRecord(filled, ks);
+            if (err == hipSuccess) err = hipStreamWaitEvent(stream, filled, 0);
+            for (size_t i = 0; i < units.size() && err == hipSuccess; ++i) err = copy_unit(units[i], slot, l, false);
+            if (err == hipSuccess) err = hipEventRecord(freed, stream);
+        }
+        if (err != hipSuccess) return fail_hip(err, fn);
+        units.clear();
+        used = 0;
+        ++chunk;
+        return KVIO_OK;
+    };
+    for (int32_t l = l0; l < l1; ++l) {
+        for (int32_t s = 0; s < n; ++s) {
+            const int64_t T = rs[size_t(s)].num_tokens;
+            int64_t t0 = 0;
+            while (t0 < T) {
+                const int64_t room = (cap - used) / (2 * R);
+                const int64_t take = T - t0 <= room ? T - t0 : room / P * P;
+                if (take == 0 || units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
+                    if (units.empty()) return fail(KVIO_EINVAL, "%s: staging slot below one page", fn);
+                    kvio_status st = flush(l);
+                    if (st != KVIO_OK) return st;
+                    continue;
+                }
+                units.push_back({s, t0, take, used});
+                used += 2 * take * R;
+                t0 += take;
+            }
+        }
+        kvio_status st = flush(l);
+        if (st != KVIO_OK) return st;
+    }
+    if (dir == kvio::kLoad && chunk > 0) {
+        e = hipEventRecord(p->ev_done[dir], ks);
+        if (e == hipSuccess) e = hipStreamWaitEvent(stream, p->ev_done[dir], 0);
+        if (e != hipSuccess) return fail_hip(e, fn);
+    }
+    return KVIO_OK;
+}
+
 kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
                      hipStream_t stream, kvio::Direction dir, const char *fn) {
     g_last_error.clear();
@@ -332,6 +548,7 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
     kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
     if (st != KVIO_OK) return st;
     const kvio_launch &lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
+    if (lc.flags & KVIO_LAUNCH_STAGED) return run_staged(p, rs, spans, n, l0, l1, stream, dir, resolve(lc, kDefaultStaged), fn);
     kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kDefaultLoad : kDefaultOffload);
     const int64_t R = p->row_bytes;
     // LDS staging of a head-major tile needs the whole tile (>= one row) in the
@@ -354,7 +571,6 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
         a.vec_shift = ilog2_exact(R / 16);
         a.rows_per_tile = rpt;
         a.n_spans = cnt;
-        a.span_base = first;
         a.host_layout = p->host_layout;
         a.num_heads = p->num_heads;
         a.seg_vecs = static_cast<int32_t>(p->seg_bytes / 16);
@@ -366,6 +582,7 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
             a.spans[i].page_idx = r.page_idx;
             a.spans[i].host_tokens = r.host_tokens;
             a.spans[i].num_tokens = static_cast<int32_t>(r.num_tokens);
+            a.spans[i].origin = first + i;
             tiles += (r.num_tokens + rpt - 1) / rpt;
         }
         a.tile_prefix[cnt] = tiles;

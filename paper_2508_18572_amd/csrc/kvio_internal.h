@@ -15,6 +15,8 @@ struct SpanArg {
     const int32_t *page_idx;   // device page table
     int64_t host_tokens;       // per-(layer, K|V) token stride of the chunk
     int32_t num_tokens;        // tokens to move, < 2^31
+    int32_t origin;            // index of the caller's span (error records)
+    int32_t page_base;         // context page of this span's first page (error records)
     int32_t pad_;
 };
 
@@ -42,7 +44,6 @@ struct CopyArgs {
     int32_t vec_shift;             // log2(V) when V is a power of two, else -1
     int32_t rows_per_tile;         // 1 .. 64
     int32_t n_spans;               // spans in this launch, 1 .. KVIO_MAX_SPANS_PER_LAUNCH
-    int32_t span_base;             // index of spans[0] in the caller's span array
     int32_t host_layout;           // KVIO_HOST_*
     int32_t num_heads;             // H (head-major chunks)
     int32_t seg_vecs;              // De / 16, 16-byte vectors per head segment (head-major)

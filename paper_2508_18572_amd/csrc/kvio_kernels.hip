@@ -90,7 +90,7 @@ __device__ __forceinline__ TileLoc locate(const CopyArgs &a, int64_t g) {
 
 // Lane r < nrows: pool slot of token t0 + r, or -1 for rows past the tile or
 // an out-of-range page (recorded once in the error word, never dereferenced).
-__device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp, int span,
+__device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp,
                                          int64_t t0, int nrows, int lane) {
     int slot = -1;
     if (lane < nrows) {
@@ -108,8 +108,8 @@ __device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp, i
             slot = static_cast<int>(static_cast<int64_t>(page) * a.page_size + off);
         } else {
             const unsigned long long code =
-                (static_cast<unsigned long long>(a.span_base + span + 1) << kErrSpanShift) |
-                static_cast<unsigned long long>(cpage);
+                (static_cast<unsigned long long>(sp.origin + 1) << kErrSpanShift) |
+                static_cast<unsigned long long>(sp.page_base + cpage);
             atomicCAS(a.err, 0ull, code);
         }
     }
@@ -301,7 +301,7 @@ __global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBo
             // First byte of the tile's rows (layer-major chunk, K then V).
             host += ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * sp.host_tokens + loc.t0) * a.row_bytes;
         }
-        const int slot = lane_slot(a, sp, loc.span, loc.t0, loc.nrows, lane);
+        const int slot = lane_slot(a, sp, loc.t0, loc.nrows, lane);
         const int nvec = loc.nrows * a.vec_per_row;
 #pragma unroll 1
         for (int base = 0; base < nvec; base += 64 * U) {
@@ -357,7 +357,7 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
         uint8_t *host = const_cast<uint8_t *>(sp.host) +
                         ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * a.num_heads * sp.host_tokens + loc.t0) * De;
         const int64_t head_stride = sp.host_tokens * De;
-        const int slot = lane_slot(a, sp, loc.span, loc.t0, n, lane);
+        const int slot = lane_slot(a, sp, loc.t0, n, lane);
         const int nvec = n * V;
 #pragma unroll 1
         for (int base = 0; base < nvec; base += 64 * U) {

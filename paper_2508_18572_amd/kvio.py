@@ -36,6 +36,7 @@ KVIO_HOST_PAGE_FIRST = 1
 KVIO_HOST_HEAD_MAJOR = 2
 KVIO_LAUNCH_CACHED = 0x1
 KVIO_LAUNCH_NO_LDS = 0x2
+KVIO_LAUNCH_STAGED = 0x4
 KVIO_EIO = -7
 KVIO_DISK_PAGE_FIRST = 0
 KVIO_DISK_LAYER_FIRST = 1
@@ -56,7 +57,8 @@ class kvio_pool_desc(ctypes.Structure):
                 ("num_slots", ctypes.c_int64),
                 ("k_layers", ctypes.POINTER(ctypes.c_void_p)),
                 ("v_layers", ctypes.POINTER(ctypes.c_void_p)),
-                ("load_launch", kvio_launch), ("offload_launch", kvio_launch)]
+                ("load_launch", kvio_launch), ("offload_launch", kvio_launch),
+                ("staging_bytes", ctypes.c_int64)]
 
 
 class kvio_span(ctypes.Structure):
@@ -192,14 +194,14 @@ def kvio_pool_create(num_layers: int, num_kv_heads: int, head_dim: int, elem_byt
                      page_size: int, num_slots: int, k_layers: Sequence[int], v_layers: Sequence[int],
                      load_launch: Optional[kvio_launch] = None,
                      offload_launch: Optional[kvio_launch] = None,
-                     host_layout: int = KVIO_HOST_TOKEN_MAJOR) -> int:
+                     host_layout: int = KVIO_HOST_TOKEN_MAJOR, staging_bytes: int = 0) -> int:
     """Create a pool handle; k_layers / v_layers are device pointers (ints)."""
     kt = (ctypes.c_void_p * len(k_layers))(*k_layers)
     vt = (ctypes.c_void_p * len(v_layers))(*v_layers)
     d = kvio_pool_desc(num_layers, num_kv_heads, head_dim, elem_bytes, page_size, host_layout,
                        num_slots, ctypes.cast(kt, ctypes.POINTER(ctypes.c_void_p)),
                        ctypes.cast(vt, ctypes.POINTER(ctypes.c_void_p)),
-                       load_launch or kvio_launch(), offload_launch or kvio_launch())
+                       load_launch or kvio_launch(), offload_launch or kvio_launch(), staging_bytes)
     h = ctypes.c_void_p()
     _check(_lib.kvio_pool_create(ctypes.byref(d), ctypes.byref(h)))
     return h.value
@@ -402,7 +404,7 @@ class KVPool:
 
     def __init__(self, pool: "torch.Tensor", page_size: int,
                  load_launch: Optional[kvio_launch] = None, offload_launch: Optional[kvio_launch] = None,
-                 host_layout: int = KVIO_HOST_TOKEN_MAJOR):
+                 host_layout: int = KVIO_HOST_TOKEN_MAJOR, staging_bytes: int = 0):
         assert pool.is_cuda and pool.is_contiguous() and pool.dim() == 5 and pool.shape[0] == 2
         _, L, S, H, D = pool.shape
         self.tensor = pool
@@ -411,7 +413,7 @@ class KVPool:
         self.handle = kvio_pool_create(L, H, D, pool.element_size(), page_size, S,
                                        [pool[0, l].data_ptr() for l in range(L)],
                                        [pool[1, l].data_ptr() for l in range(L)],
-                                       load_launch, offload_launch, host_layout)
+                                       load_launch, offload_launch, host_layout, staging_bytes)
 
     def load(self, spans, layer_begin=0, layer_end=None, stream=None):
         kvio_load(self.handle, spans, layer_begin, self.num_layers if layer_end is None else layer_end, stream)

@@ -56,6 +56,18 @@ def test_host_side_validation_without_device():
     with pytest.raises(kv.KvioError) as e:
         kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], offload_launch=kv.launch(tile_kib=5))
     assert e.value.status == kv.KVIO_EINVAL
+    staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
+    with pytest.raises(kv.KvioError) as e:                      # staged: token-major chunks only
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], load_launch=staged,
+                            host_layout=kv.KVIO_HOST_PAGE_FIRST)
+    assert e.value.status == kv.KVIO_EINVAL and "token-major" in e.value.detail
+    with pytest.raises(kv.KvioError) as e:                      # staging below one page of K and V rows
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], offload_launch=staged,
+                            staging_bytes=2 * 16 * 512 - 16)
+    assert e.value.status == kv.KVIO_EINVAL and "staging_bytes" in e.value.detail
+    with pytest.raises(kv.KvioError) as e:                      # unknown flag bit
+        kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], load_launch=kv.launch(flags=0x80))
+    assert e.value.status == kv.KVIO_EINVAL
     with pytest.raises(kv.KvioError) as e:                      # null pool handle
         kv.kvio_load(0, [], 0, 1)
     assert e.value.status == kv.KVIO_EINVAL

@@ -38,7 +38,7 @@ def _pool_bytes(pool_t):
     return pool_t.cpu().numpy().view(np.uint8).reshape(2, L, S, -1)
 
 
-def run_case(kv, L, H, D, P, S, spans, l0=0, l1=None, launch=None, seed=0, shape=W.LLAMA8B):
+def run_case(kv, L, H, D, P, S, spans, l0=0, l1=None, launch=None, seed=0, shape=W.LLAMA8B, staging_bytes=0):
     """spans: list of (num_tokens, host_tokens).  Loads, checks, offloads, checks."""
     import torch
     l1 = L if l1 is None else l1
@@ -66,7 +66,7 @@ def run_case(kv, L, H, D, P, S, spans, l0=0, l1=None, launch=None, seed=0, shape
             ora_out.append(eo)
             dev_spans.append((hb.ptr, HT, T, pt.data_ptr()))
             dev_out.append((ob.ptr, HT, T, pt.data_ptr()))
-        pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
+        pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch, staging_bytes=staging_bytes)
         # load
         pool.load(dev_spans, l0, l1)
         torch.cuda.synchronize()
@@ -129,6 +129,120 @@ def test_parity_launch_shapes(kv, wg, threads, tile, flags):
     run_case(kv, 2, 8, 128, 1, 3000, [(777, 800), (3, 3)], launch=launch, seed=wg)
     run_case(kv, 2, 4, 64, 16, 4096, [(1000, 1024)], launch=launch, seed=wg + 1)
     run_case(kv, 1, 1, 8, 3, 300, [(70, 80)], launch=launch, seed=wg + 2)
+
+
+def _staging(slot_pages, P, R):
+    """staging_bytes whose 4 slots hold slot_pages pages of K and V rows each
+    (0 = the library default), plus a few bytes the library rounds away."""
+    return 0 if slot_pages == 0 else 4 * slot_pages * 2 * P * R + 48
+
+
+@pytest.mark.parametrize("slot_pages", [0, 1, 3, 10])
+def test_parity_staged(kv, slot_pages):
+    """KVIO_LAUNCH_STAGED: copy-engine copies through HBM staging slots and a
+    scatter / gather kernel.  Small slots split spans into units of whole
+    pages and cycle the four slots many times per call."""
+    for flags in (kv.KVIO_LAUNCH_STAGED, kv.KVIO_LAUNCH_STAGED | kv.KVIO_LAUNCH_CACHED):
+        launch = kv.launch(flags=flags)
+        run_case(kv, 2, 8, 128, 16, 4096, [(1000, 1024), (333, 400), (0, 5), (17, 17)], launch=launch,
+                 seed=40 + flags, staging_bytes=_staging(slot_pages, 16, 2048))
+        run_case(kv, 3, 8, 128, 1, 5000, [(1000, 1200), (1, 1)], l0=1, l1=3, launch=launch, seed=41,
+                 staging_bytes=_staging(slot_pages, 1, 2048))
+        run_case(kv, 1, 1, 8, 3, 300, [(70, 80), (5, 9)], launch=launch, seed=42,
+                 staging_bytes=_staging(slot_pages, 3, 16))
+        run_case(kv, 2, 6, 128, 2, 600, [(201, 250)], launch=launch, seed=43,
+                 staging_bytes=_staging(slot_pages, 2, 1536))
+    # small scatter launches and every tile size
+    for wg, th, tile in ((1, 64, 4), (7, 256, 8), (64, 512, 16)):
+        run_case(kv, 2, 4, 64, 16, 4096, [(1000, 1024)], launch=kv.launch(wg, th, tile, kv.KVIO_LAUNCH_STAGED),
+                 seed=44 + wg, staging_bytes=_staging(slot_pages, 16, 512))
+
+
+def test_parity_staged_many_spans(kv):
+    # 70 contexts: more units than one scatter launch carries
+    rng = np.random.default_rng(19)
+    spans = [(int(t), int(t) + int(e)) for t, e in zip(rng.integers(0, 40, 70), rng.integers(0, 3, 70))]
+    run_case(kv, 2, 8, 128, 16, 4096, spans, launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED), seed=19)
+    run_case(kv, 2, 8, 128, 16, 4096, spans, launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED), seed=20,
+             staging_bytes=_staging(2, 16, 2048))
+
+
+def test_staged_calls_keep_stream_order(kv):
+    """Staged offload, then staged load of the same host chunk into other
+    pages, then an offload of those pages, all queued on one stream with no
+    host synchronisation: each call must see the previous one's results (the
+    copies of one run on the pool's own copy streams)."""
+    import torch
+    L, H, D, P, S, T = 4, 8, 128, 16, 4096, 1000
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 23)
+    rng = np.random.default_rng(23)
+    need = -(-T // P)
+    perm = rng.permutation(S // P)[:2 * need].astype(np.int32)
+    pa, pb = torch.from_numpy(perm[:need].copy()).cuda(), torch.from_numpy(perm[need:].copy()).cuda()
+    staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
+    with kv.HostBuffer(L * 2 * T * R) as mid, kv.HostBuffer(L * 2 * T * R) as out:
+        mid.array[:] = 0
+        out.array[:] = 0
+        pool = kv.KVPool(pool_t, P, load_launch=staged, offload_launch=staged, staging_bytes=_staging(3, P, R))
+        s = torch.cuda.Stream()
+        for _ in range(2):
+            pool.offload([(mid.ptr, T, T, pa.data_ptr())], stream=s)     # pages A -> mid
+            pool.load([(mid.ptr, T, T, pb.data_ptr())], stream=s)        # mid -> pages B
+            pool.offload([(out.ptr, T, T, pb.data_ptr())], stream=s)     # pages B -> out
+        s.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        e_mid = np.zeros(L * 2 * T * R, np.uint8)
+        oracle.offload(exp[0], exp[1], P, [(e_mid, T, T, perm[:need])])
+        oracle.load(exp[0], exp[1], P, [(e_mid, T, T, perm[need:])])
+        assert np.array_equal(mid.array, e_mid)
+        assert np.array_equal(out.array, e_mid)
+        assert np.array_equal(_pool_bytes(pool_t), exp)
+        pool.close()
+
+
+def test_staged_layer_call_and_errors(kv):
+    """kvio_load_layer in staged mode, its event, and an out-of-range page
+    reported with the caller's span and context page although the span was
+    split into staging units."""
+    import torch
+    L, H, D, P, S = 3, 8, 128, 16, 2048
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 21)
+    T = 200
+    pages = np.random.default_rng(21).permutation(S // P)[:-(-T // P)].astype(np.int32)
+    pt = torch.from_numpy(pages.copy()).cuda()
+    staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
+    with kv.HostBuffer(L * 2 * T * R) as hb:
+        W.fill_np(hb.array, 21, W.LLAMA8B)
+        pool = kv.KVPool(pool_t, P, load_launch=staged, offload_launch=staged, staging_bytes=_staging(2, P, R))
+        s = torch.cuda.Stream()
+        ev = torch.cuda.Event()
+        for l in range(L):
+            pool.load_layer([(hb.ptr, T, T, pt.data_ptr())], l, stream=s, done=ev)
+        ev.synchronize()
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, [(hb.array, T, T, pages)])
+        assert np.array_equal(_pool_bytes(pool_t), exp)
+        bad = pages.copy()
+        bad[9] = S // P + 5                                  # context page 9 of span 1 is out of range
+        pb = torch.from_numpy(bad).cuda()
+        pool.load([(hb.ptr, T, 0, pt.data_ptr()), (hb.ptr, T, T, pb.data_ptr())])
+        torch.cuda.synchronize()
+        with pytest.raises(kv.KvioError) as e:
+            pool.check()
+        assert e.value.status == kv.KVIO_ERANGE
+        assert "span 1" in e.value.detail and "context page 9" in e.value.detail, e.value.detail
+        pool.close()
+    with pytest.raises(kv.KvioError) as e:                  # slots smaller than one page of K and V
+        kv.KVPool(pool_t, P, load_launch=staged, staging_bytes=4 * 2 * P * R - 16)
+    assert e.value.status == kv.KVIO_EINVAL
+    with pytest.raises(kv.KvioError) as e:                  # staged transfers take token-major chunks only
+        kv.KVPool(pool_t, P, offload_launch=staged, host_layout=kv.KVIO_HOST_PAGE_FIRST)
+    assert e.value.status == kv.KVIO_EINVAL
 
 
 def test_torch_pinned_host_memory(kv):
