@@ -108,3 +108,28 @@ def test_rounds_drain_any_queue():
         # the rest keeps queue order
         assert [r.rid for r in cur] == sorted(rest, key=lambda i: [x.rid for x in q].index(i))
     assert sorted(seen) == list(range(40))
+
+
+def test_deferred_requests_go_to_the_front():
+    # Sec. 4.3.1: a deferred request waits for the next round at the FRONT of the queue,
+    # ahead of eligible requests this round could not take
+    q = [Request(0, 0, 100, transient_matches=500), Request(1, 0, 100), Request(2, 0, 100)]
+    batch, nxt = schedule_round(q, max_tokens=10**6, max_requests=1)
+    assert batch == [1] and nxt == [0, 2]
+
+
+def test_budget_reached_exactly_is_full():
+    # a batch whose compute tokens reach the budget exactly is full (reading of is_full)
+    q = [Request(0, 0, 400), Request(1, 0, 600), Request(2, 0, 100)]
+    batch, rest = batch_formation(q, max_tokens=1_000, max_requests=64)
+    assert batch == [0, 1] and rest == [2]
+
+
+def test_shared_context_loads_once():
+    # A and its bundle hit B share context 1: the batch loads 1000 tokens, not 2000.
+    # C then keeps the batch at 2000 / 25 = 80 <= 100 and joins (full at 3 requests);
+    # counting the shared context twice would give 3000 / 25 = 120 and let D in instead.
+    q = [Request(0, 1000, 10, context=1), Request(1, 1000, 10, context=1), Request(2, 1000, 5),
+         Request(3, 0, 5)]
+    batch, rest = batch_formation(q, max_tokens=10**6, max_requests=3)
+    assert batch == [0, 1, 2] and rest == [3]
