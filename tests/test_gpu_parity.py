@@ -245,6 +245,30 @@ def test_staged_layer_call_and_errors(kv):
     assert e.value.status == kv.KVIO_EINVAL
 
 
+@pytest.mark.parametrize("flags", [0, 0x4])
+def test_empty_batches_are_no_ops(kv, flags):
+    """No spans, or spans with no tokens, in every call: nothing moves and
+    nothing is reported (plain and staged launches)."""
+    import torch
+    L, H, D, P, S = 2, 8, 128, 16, 1024
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 30)
+    launch = kv.launch(flags=flags)
+    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
+    pt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    with kv.HostBuffer(L * 2 * 16 * R) as hb:
+        hb.array[:] = 0x77
+        for spans in ([], [(hb.ptr, 16, 0, pt.data_ptr())], [(hb.ptr, 0, 0, pt.data_ptr())] * 3):
+            pool.load(spans)
+            pool.offload(spans)
+            pool.load_layer(spans, L - 1)
+        torch.cuda.synchronize()
+        pool.check()
+        assert np.array_equal(_pool_bytes(pool_t), pool_np)
+        assert (hb.array == 0x77).all()
+    pool.close()
+
+
 def test_torch_pinned_host_memory(kv):
     """Host chunks from torch's pinned allocator work like kvio_host_alloc ones."""
     import torch
