@@ -190,14 +190,15 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
         res[name] = nbytes / (statistics.median(t.ms()) * 1e-3) / GB
     # bidirectional: H2D of one half while D2H of the other half.  Copies on
     # two ordinary streams can serialise (they may share a hardware queue);
-    # pairs that include the transfer stream (a queue of its own) or the null
-    # stream run concurrently, but not reliably on every run, so several such
-    # pairs are tried and the best (the link's real bidirectional capacity)
-    # is kept.
+    # a pair of the transfer stream (or the null stream) with a stream made
+    # before the transfer stream runs concurrently, later-made streams do so
+    # only on some runs.  Several pairs are tried and the best (the link's
+    # real bidirectional capacity) is kept.
     best = 0.0
     null = torch.cuda.default_stream()
-    pairs = [(s1, s2)] + [(s1, torch.cuda.Stream()) for _ in range(3)] + \
-            [(null, torch.cuda.Stream()) for _ in range(3)] + [(torch.cuda.Stream(), null)]
+    early = _PEAK.get("early_streams", [])
+    pairs = [(s1, e) for e in early] + [(null, e) for e in early] + [(s1, s2)] + \
+            [(s1, torch.cuda.Stream()) for _ in range(2)] + [(null, torch.cuda.Stream()) for _ in range(2)]
     for a, b in pairs:
         ts = []
         for _ in range(reps):
@@ -1139,8 +1140,8 @@ def main():
         return
     k = args.config
     try:
-        # the transfer stream first: streams created later (the pool's own
-        # copy streams among them) then take the remaining hardware queues
+        # a few plain streams for the bidirectional peak, then the transfer stream
+        _PEAK["early_streams"] = [torch.cuda.Stream() for _ in range(3)]
         io_stream(torch, kv)
         if not args.no_peak and not args.disk and not args.schedule:
             h2d_d2h_peak(torch, kv)
