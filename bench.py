@@ -98,7 +98,9 @@ def parse():
 
 def measured_traffic(config, default_launch):
     """HBM/link bytes per load launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel sources (else None)."""
+    summary, if it was taken on the current kernels: the kernel source and
+    the header that holds the kernel arguments and default launch shapes
+    (else None)."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "kvio_copy_kernel__llama8b_p1_32k.counters.txt")
     if config != 2 or not default_launch or not os.path.exists(path):
@@ -110,7 +112,7 @@ def measured_traffic(config, default_launch):
             kv[key.strip()] = val.strip()
     csrc = os.path.join(ROOT, "paper_2508_18572_amd", "csrc")
     cur = " ".join(hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest()
-                   for f in ("kvio_kernels.hip", "kvio_internal.h", "kvio_api.cpp"))
+                   for f in ("kvio_kernels.hip", "kvio_internal.h"))
     if cur != kv.get("kernel_sources_sha256"):
         return None
     fetch = float(kv["load_fetch_kib"]) * float(kv["fetch_scale"]) * 1024

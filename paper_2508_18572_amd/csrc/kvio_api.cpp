@@ -1,7 +1,8 @@
 // kvio_api.cpp -- the C ABI of libkvio.so: validation, pool handles, launch
-// shaping, the naive per-page DMA baseline and thread-local error text.
-// Every data-moving step of kvio_load / kvio_offload runs in the kernels of
-// kvio_kernels.hip; this file only checks arguments and enqueues them.
+// shaping, staged transfers, the naive per-page DMA baseline and thread-local
+// error text.  Every layout-converting step of kvio_load / kvio_offload runs
+// in the kernels of kvio_kernels.hip; this file checks arguments and enqueues
+// them (staged launches also enqueue copy-engine copies of contiguous runs).
 #include <hip/hip_runtime.h>
 
 #include <stdarg.h>
@@ -41,18 +42,6 @@ int ilog2_exact(int64_t v) {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Library defaults for the launch shape, chosen by measurement on MI355X
-// (PCIe Gen5 x16 host link).  Load: 16 workgroups x 4 waves with 4 KiB steps
-// saturate the link (57.6 GB/s at page size 1, the contiguous memcpy peak),
-// reach 90% of it on a 2 MiB context, and leave 240 of 256 CUs to co-running
-// compute.  Offload: 32 workgroups x 4 waves with 16 KiB steps (55.6 GB/s).
-constexpr int kDefaultThreads = 256;
-constexpr kvio::Shape kDefaultLoad = {16, kDefaultThreads, 4, true, true};
-constexpr kvio::Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
-// Staged transfers: the scatter / gather between the HBM staging buffer and
-// the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at
-// page size 1 in 1.75 ms, 2.4 TB/s of payload).
-constexpr kvio::Shape kDefaultStaged = {1024, kDefaultThreads, 16, true, true};
 constexpr int64_t kDefaultStagingBytes = int64_t(1) << 30;
 // The staging buffer is split into this many slots so the copy engine fills
 // (drains) one while the kernel scatters (gathers) another.
@@ -548,8 +537,8 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
     kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
     if (st != KVIO_OK) return st;
     const kvio_launch &lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
-    if (lc.flags & KVIO_LAUNCH_STAGED) return run_staged(p, rs, spans, n, l0, l1, stream, dir, resolve(lc, kDefaultStaged), fn);
-    kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kDefaultLoad : kDefaultOffload);
+    if (lc.flags & KVIO_LAUNCH_STAGED) return run_staged(p, rs, spans, n, l0, l1, stream, dir, resolve(lc, kvio::kDefaultStaged), fn);
+    kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);
     const int64_t R = p->row_bytes;
     // LDS staging of a head-major tile needs the whole tile (>= one row) in the
     // wave's U KiB slice.

@@ -62,6 +62,19 @@ struct Shape {
     bool head_major_lds;  // head-major chunks: stage the transpose through LDS
 };
 
+// Library defaults for the launch shape, chosen by measurement on MI355X
+// (PCIe Gen5 x16 host link).  Load: 16 workgroups x 4 waves with 4 KiB steps
+// saturate the link (57.6 GB/s at page size 1, the contiguous memcpy peak),
+// reach 90% of it on a 2 MiB context, and leave 240 of 256 CUs to co-running
+// compute.  Offload: 32 workgroups x 4 waves with 16 KiB steps (55.6 GB/s).
+constexpr int kDefaultThreads = 256;
+constexpr Shape kDefaultLoad = {16, kDefaultThreads, 4, true, true};
+constexpr Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
+// Staged transfers: the scatter / gather between the HBM staging buffer and
+// the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at
+// page size 1 in 1.75 ms, 2.4 TB/s of payload).
+constexpr Shape kDefaultStaged = {1024, kDefaultThreads, 16, true, true};
+
 // Rows per tile for a given step size: one step moves tile_kib KiB per wave.
 int rows_per_tile(int64_t row_bytes, int tile_kib);
 
