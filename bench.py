@@ -557,8 +557,9 @@ def run_bidirectional(args, torch, kv, W):
     bg = [int(x) for x in args.bg_offload.split(",")]
     # a second handle on the same pool whose offloads run with the background quota
     pool_bg = kv.KVPool(pool_t, P, offload_launch=kv.launch(bg[0], bg[1], bg[2], 0))
-    host = kv.HostBuffer(nb)
-    src_o, dst_o = kv.HostBuffer(nbo), kv.HostBuffer(nbo)
+    hflags = kv.KVIO_HOST_NONCOHERENT if args.noncoherent_host else kv.KVIO_HOST_COHERENT
+    host = kv.HostBuffer(nb, hflags)
+    src_o, dst_o = kv.HostBuffer(nbo, hflags), kv.HostBuffer(nbo, hflags)
     peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
     W.fill_cuda(host.ptr, nb, W.data_seed(k), shp)
     W.fill_cuda(src_o.ptr, nbo, W.data_seed(k) * 1000 + 1, shp)
