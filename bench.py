@@ -946,17 +946,30 @@ def run_schedule(args, torch, kv, W):
         f"{prefill_tok_s:.0f} prefill tokens/s; loading-bound when load tokens > {cost_ratio:.2f} x compute tokens")
 
     # ---- (1) host cost of one scheduling round ---------------------------------------------
+    import ctypes
+    from paper_2508_18572_amd import kvio as kvmod
     cost = {}
     for n in (64, 1024, 16384):
         q = synthetic_queue(n, 700 + n)
-        kv.kvio_schedule_round(q, 8192, 16)
-        reps = 200 if n <= 1024 else 20
+        arr = (kvmod.kvio_request * n)()
+        for i, (ld, cp, cx, m) in enumerate(q):
+            arr[i] = kvmod.kvio_request(ld, cp, -1 if cx is None else cx, m)
+        pol = kvmod.kvio_batch_policy(8192, 16, 0, 0.0, -1)
+        bout, qout = (ctypes.c_int32 * n)(), (ctypes.c_int32 * n)()
+        nb_, nq_ = ctypes.c_int32(), ctypes.c_int32()
+        reps = max(5, 20000 // n)
         c0 = time.perf_counter()
-        for _ in range(reps):
+        for _ in range(reps):                    # the C call alone, arrays already built
+            kvmod._lib.kvio_schedule_round(arr, n, ctypes.byref(pol), bout, ctypes.byref(nb_), qout,
+                                           ctypes.byref(nq_))
+        raw = (time.perf_counter() - c0) / reps * 1e6
+        c0 = time.perf_counter()
+        for _ in range(reps):                    # through the Python binding (marshalling included)
             kv.kvio_schedule_round(q, 8192, 16)
-        cost[n] = (time.perf_counter() - c0) / reps * 1e6
-    log("scheduling round (incl. ctypes marshalling): " + ", ".join(f"{n} requests {u:.1f} us"
-                                                                   for n, u in cost.items()))
+        cost[n] = {"c_call_us": round(raw, 2), "with_python_marshalling_us": round((time.perf_counter() - c0) / reps * 1e6, 2)}
+    log("scheduling round: " + ", ".join(f"{n} requests {c['c_call_us']:.1f} us in C "
+                                         f"({c['with_python_marshalling_us']:.1f} us through Python)"
+                                         for n, c in cost.items()))
 
     # ---- (2) FIFO vs Algorithm 1 under the measured cost model -------------------------------
     sim = {}
@@ -981,7 +994,7 @@ def run_schedule(args, torch, kv, W):
     res["rates"] = {"kvio_load_gbps": round(load_gbps, 3), "load_tokens_per_s": round(load_tok_s, 1),
                     "gemm_tflops": round(gemm_tflops, 1), "prefill_tokens_per_s": round(prefill_tok_s, 1),
                     "cost_model_ratio": round(cost_ratio, 3)}
-    res["schedule_round_us"] = {str(n): round(u, 2) for n, u in cost.items()}
+    res["schedule_round"] = {str(n): c for n, c in cost.items()}
     res["simulation"] = sim
     print(json.dumps(res), flush=True)
 
