@@ -138,7 +138,7 @@ typedef struct kvio_pool_desc {
     kvio_launch offload_launch; /* launch shape of offload kernels                       */
     int64_t staging_bytes;    /* HBM staging per direction with KVIO_LAUNCH_STAGED: 4 slots
                                  of staging_bytes / 4 (rounded down to 16 B), each >= 2 * P
-                                 * R; 0 = 1 GiB.  Allocated by kvio_pool_create, with a
+                                 * R; 0 = 4 GiB.  Allocated by kvio_pool_create, with a
                                  side stream and events, only for staged directions.      */
 } kvio_pool_desc;
 

@@ -9,6 +9,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -42,7 +43,7 @@ int ilog2_exact(int64_t v) {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-constexpr int64_t kDefaultStagingBytes = int64_t(1) << 30;
+constexpr int64_t kDefaultStagingBytes = int64_t(4) << 30;
 // The staging buffer is split into this many slots so the copy engine fills
 // (drains) one while the kernel scatters (gathers) another.
 constexpr int kStageSlots = 4;
@@ -408,22 +409,24 @@ hipError_t launch_capped(const kvio::CopyArgs &a, kvio::Direction dir, kvio::Sha
     return kvio::launch_copy(a, dir, s, stream);
 }
 
-// Staged transfer (KVIO_LAUNCH_STAGED).  Layer by layer, the spans' token
-// runs are packed into staging slots as units of n tokens: K rows
-// [t0, t0 + n) then V rows; a unit is as many tokens as fit (a multiple of P
-// unless it ends the span).  The copy engine works on the caller's stream,
-// the scatter / gather kernel on the pool's kernel stream for this
-// direction; events hand each slot over:
+// Staged transfer (KVIO_LAUNCH_STAGED).  Work is packed into staging slots as
+// units: span s, tokens [t0, t0 + n), layers [lb, lb + g) (shared by every
+// unit of a slot), laid out like a chunk of n tokens: row (l, kv, t) at
+// ((l - lb)*2 + kv)*n*R + (t - t0)*R from the unit.  When one layer of every
+// span fits a slot, units are whole spans over as many layers as fit, and a
+// span whose planes are contiguous (num_tokens == host_tokens) moves with one
+// copy; otherwise layer by layer, spans split into runs of whole pages.  The
+// copy engine works on the caller's stream, the scatter / gather kernel on
+// the pool's side stream for this direction; events hand each slot over:
 //   load:    caller: [wait slot free] copies in -> filled
-//            kernel: wait filled -> scatter -> slot free
-//   offload: kernel: [wait slot free] gather -> filled
+//            side:   wait filled -> scatter -> slot free
+//   offload: side:   [wait slot free] gather -> filled
 //            caller: wait filled -> copies out -> slot free
-// An offload's kernel stream first waits for the work already on the
-// caller's stream (the pool rows it reads may come from it); a load ends
-// with the caller's stream waiting for the last scatter.  So the call keeps
-// stream order.  The kernel sees each unit as a one-layer span whose chunk
-// starts l*2*n*R bytes before the unit, so its usual row address
-// ((l*2 + kv)*n + t)*R lands inside the unit.
+// An offload's side stream first waits for the work already on the caller's
+// stream (the pool rows it reads may come from it); a load ends with the
+// caller's stream waiting for the last scatter.  So the call keeps stream
+// order.  The kernel sees a unit as a span whose chunk starts lb*2*n*R bytes
+// before it, so its usual row address ((l*2 + kv)*n + t)*R lands inside.
 kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvio_span *spans, int32_t n,
                        int32_t l0, int32_t l1, hipStream_t stream, kvio::Direction dir, const kvio::Shape &shape,
                        const char *fn) {
@@ -440,19 +443,25 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
         if (e == hipSuccess) e = hipStreamWaitEvent(ks, p->ev_start[dir], 0);
         if (e != hipSuccess) return fail_hip(e, fn);
     }
-    auto copy_unit = [&](const Unit &u, uint8_t *slot, int32_t l, bool to_stage) -> hipError_t {
+    // Host <-> slot copies of one unit over layers [lb, lb + g).
+    auto copy_unit = [&](const Unit &u, uint8_t *slot, int32_t lb, int32_t g, bool to_stage) -> hipError_t {
         uint8_t *host = static_cast<uint8_t *>(spans[u.span].host);
         const int64_t ht = spans[u.span].host_tokens;
-        for (int kv = 0; kv < 2; ++kv) {
-            uint8_t *h = host + ((int64_t(l) * 2 + kv) * ht + u.t0) * R;
-            uint8_t *d = slot + u.off + kv * u.n * R;
-            hipError_t err = to_stage ? hipMemcpyAsync(d, h, size_t(u.n * R), hipMemcpyHostToDevice, stream)
-                                      : hipMemcpyAsync(h, d, size_t(u.n * R), hipMemcpyDeviceToHost, stream);
-            if (err != hipSuccess) return err;
-        }
+        auto one = [&](uint8_t *h, uint8_t *d, int64_t bytes) {
+            return to_stage ? hipMemcpyAsync(d, h, size_t(bytes), hipMemcpyHostToDevice, stream)
+                            : hipMemcpyAsync(h, d, size_t(bytes), hipMemcpyDeviceToHost, stream);
+        };
+        if (u.t0 == 0 && u.n == ht)           // whole planes: one contiguous run
+            return one(host + int64_t(lb) * 2 * ht * R, slot + u.off, int64_t(g) * 2 * u.n * R);
+        for (int32_t l = lb; l < lb + g; ++l)
+            for (int kv = 0; kv < 2; ++kv) {
+                hipError_t err = one(host + ((int64_t(l) * 2 + kv) * ht + u.t0) * R,
+                                     slot + u.off + ((int64_t(l - lb) * 2 + kv) * u.n) * R, u.n * R);
+                if (err != hipSuccess) return err;
+            }
         return hipSuccess;
     };
-    auto flush = [&](int32_t l) -> kvio_status {
+    auto flush = [&](int32_t lb, int32_t g) -> kvio_status {
         if (units.empty()) return KVIO_OK;
         const int k = int(chunk % kStageSlots);
         uint8_t *slot = p->stage[dir] + int64_t(k) * cap;
@@ -460,7 +469,7 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
         hipError_t err = hipSuccess;
         if (dir == kvio::kLoad) {
             if (chunk >= kStageSlots) err = hipStreamWaitEvent(stream, freed, 0);
-            for (size_t i = 0; i < units.size() && err == hipSuccess; ++i) err = copy_unit(units[i], slot, l, true);
+            for (size_t i = 0; i < units.size() && err == hipSuccess; ++i) err = copy_unit(units[i], slot, lb, g, true);
             if (err == hipSuccess) err = hipEventRecord(filled, stream);
             if (err == hipSuccess) err = hipStreamWaitEvent(ks, filled, 0);
         } else if (chunk >= kStageSlots) {
@@ -468,14 +477,14 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
         }
         if (err != hipSuccess) return fail_hip(err, fn);
         kvio::CopyArgs a;
-        common_args(p, shape, l, &a);
+        common_args(p, shape, lb, &a);
         a.n_spans = static_cast<int32_t>(units.size());
         int64_t tiles = 0;
         for (size_t i = 0; i < units.size(); ++i) {
             const Unit &u = units[i];
             a.tile_prefix[i] = tiles;
             a.spans[i].host = reinterpret_cast<const uint8_t *>(reinterpret_cast<uintptr_t>(slot) + uintptr_t(u.off) -
-                                                                uintptr_t(int64_t(l) * 2 * u.n * R));
+                                                                uintptr_t(int64_t(lb) * 2 * u.n * R));
             a.spans[i].page_idx = rs[size_t(u.span)].page_idx + u.t0 / P;
             a.spans[i].host_tokens = u.n;
             a.spans[i].num_tokens = static_cast<int32_t>(u.n);
@@ -485,14 +494,15 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
         }
         a.tile_prefix[units.size()] = tiles;
         a.plane_tiles = tiles;
-        a.total_tiles = tiles * 2;
+        a.total_tiles = tiles * 2 * g;
         if ((err = launch_capped(a, dir, shape, ks)) != hipSuccess) return fail_hip(err, fn);
         if (dir == kvio::kLoad) {
             err = hipEventRecord(freed, ks);
         } else {
             err = hipEventRecord(filled, ks);
             if (err == hipSuccess) err = hipStreamWaitEvent(stream, filled, 0);
-            for (size_t i = 0; i < units.size() && err == hipSuccess; ++i) err = copy_unit(units[i], slot, l, false);
+            for (size_t i = 0; i < units.size() && err == hipSuccess; ++i)
+                err = copy_unit(units[i], slot, lb, g, false);
             if (err == hipSuccess) err = hipEventRecord(freed, stream);
         }
         if (err != hipSuccess) return fail_hip(err, fn);
@@ -501,7 +511,29 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
         ++chunk;
         return KVIO_OK;
     };
-    for (int32_t l = l0; l < l1; ++l) {
+    int64_t layer_bytes = 0;                  // one layer of every span
+    for (int32_t s = 0; s < n; ++s) layer_bytes += 2 * rs[size_t(s)].num_tokens * R;
+    if (layer_bytes == 0) return KVIO_OK;
+    for (int32_t l = l0; l < l1;) {
+        if (layer_bytes <= cap) {
+            // whole spans over g layers per slot
+            const int32_t g = int32_t(std::min<int64_t>(l1 - l, cap / layer_bytes));
+            for (int32_t s = 0; s < n; ++s) {
+                const int64_t T = rs[size_t(s)].num_tokens;
+                if (T == 0) continue;
+                if (units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
+                    kvio_status st = flush(l, g);
+                    if (st != KVIO_OK) return st;
+                }
+                units.push_back({s, 0, T, used});
+                used += int64_t(g) * 2 * T * R;
+            }
+            kvio_status st = flush(l, g);
+            if (st != KVIO_OK) return st;
+            l += g;
+            continue;
+        }
+        // one layer per slot, spans split into runs of whole pages
         for (int32_t s = 0; s < n; ++s) {
             const int64_t T = rs[size_t(s)].num_tokens;
             int64_t t0 = 0;
@@ -510,7 +542,7 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
                 const int64_t take = T - t0 <= room ? T - t0 : room / P * P;
                 if (take == 0 || units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
                     if (units.empty()) return fail(KVIO_EINVAL, "%s: staging slot below one page", fn);
-                    kvio_status st = flush(l);
+                    kvio_status st = flush(l, 1);
                     if (st != KVIO_OK) return st;
                     continue;
                 }
@@ -519,8 +551,9 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
                 t0 += take;
             }
         }
-        kvio_status st = flush(l);
+        kvio_status st = flush(l, 1);
         if (st != KVIO_OK) return st;
+        ++l;
     }
     if (dir == kvio::kLoad && chunk > 0) {
         e = hipEventRecord(p->ev_done[dir], ks);
