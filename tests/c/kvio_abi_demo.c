@@ -72,62 +72,71 @@ static int gpu(void)
     kvio_pool_t pool = NULL;
     kvio_span span;
     uint8_t *img;
-    int i, l, kv;
+    int i, l, kv, mode;
     int64_t t;
 
     CHECK(hipMalloc((void **)&pool_dev, (size_t)(2 * L * S * R)) == hipSuccess, "hipMalloc pool");
-    CHECK(hipMemset(pool_dev, 0x5A, (size_t)(2 * L * S * R)) == hipSuccess, "hipMemset");
     CHECK(hipMalloc((void **)&pidx_dev, sizeof pidx) == hipSuccess, "hipMalloc page table");
     for (i = 0; i < npages; ++i) pidx[i] = (i * 7 + 3) % (S / P);   /* distinct pages */
     CHECK(hipMemcpy(pidx_dev, pidx, sizeof pidx, hipMemcpyHostToDevice) == hipSuccess, "page table copy");
     CHECK(kvio_host_alloc((size_t)(L * 2 * T * R), KVIO_HOST_COHERENT, (void **)&chunk) == KVIO_OK, "host alloc");
     CHECK(kvio_host_alloc((size_t)(L * 2 * T * R), KVIO_HOST_COHERENT, (void **)&out) == KVIO_OK, "host alloc");
     for (i = 0; i < L * 2 * T * R; ++i) chunk[i] = (uint8_t)(i * 131 + (i >> 9));
-    memset(out, 0xA5, (size_t)(L * 2 * T * R));
     for (l = 0; l < L; ++l) {
         kl[l] = pool_dev + (int64_t)l * S * R;
         vl[l] = pool_dev + (int64_t)(L + l) * S * R;
     }
-    memset(&d, 0, sizeof d);
-    d.num_layers = L;
-    d.num_kv_heads = H;
-    d.head_dim = D;
-    d.elem_bytes = 2;
-    d.page_size = P;
-    d.num_slots = S;
-    d.k_layers = kl;
-    d.v_layers = vl;
-    CHECK(kvio_pool_create(&d, &pool) == KVIO_OK, "pool create: %s", kvio_last_error());
-    span.host = chunk;
-    span.host_tokens = T;
-    span.num_tokens = T;
-    span.page_idx = pidx_dev;
-    CHECK(kvio_load(pool, &span, 1, 0, L, NULL) == KVIO_OK, "load: %s", kvio_last_error());
-    span.host = out;
-    CHECK(kvio_offload(pool, &span, 1, 0, L, NULL) == KVIO_OK, "offload: %s", kvio_last_error());
-    CHECK(kvio_check(pool) == KVIO_OK, "check: %s", kvio_last_error());
-    img = (uint8_t *)malloc((size_t)(2 * L * S * R));
-    CHECK(img != NULL, "malloc");
-    CHECK(hipMemcpy(img, pool_dev, (size_t)(2 * L * S * R), hipMemcpyDeviceToHost) == hipSuccess, "readback");
-    /* every moved row, by the definition; every other row still 0x5A */
-    for (l = 0; l < L; ++l)
-        for (kv = 0; kv < 2; ++kv) {
-            const uint8_t *plane = img + (int64_t)(kv * L + l) * S * R;
-            char *used = (char *)calloc(S, 1);
-            for (t = 0; t < T; ++t) {
-                const int64_t slot = (int64_t)pidx[t / P] * P + t % P;
-                const uint8_t *src = chunk + ((int64_t)(l * 2 + kv) * T + t) * R;
-                used[slot] = 1;
-                CHECK(memcmp(plane + slot * R, src, (size_t)R) == 0, "row l=%d kv=%d t=%lld", l, kv, (long long)t);
-            }
-            for (t = 0; t < S; ++t)
-                if (!used[t])
-                    for (i = 0; i < R; ++i) CHECK(plane[t * R + i] == 0x5A, "untouched slot %lld", (long long)t);
-            free(used);
+    /* mode 0: the transfer kernels read / write the pinned chunk; mode 1:
+     * staged through HBM slots (three pages of K and V rows each) */
+    for (mode = 0; mode < 2; ++mode) {
+        CHECK(hipMemset(pool_dev, 0x5A, (size_t)(2 * L * S * R)) == hipSuccess, "hipMemset");
+        memset(out, 0xA5, (size_t)(L * 2 * T * R));
+        memset(&d, 0, sizeof d);
+        if (mode == 1) {
+            d.load_launch.flags = KVIO_LAUNCH_STAGED;
+            d.offload_launch.flags = KVIO_LAUNCH_STAGED;
+            d.staging_bytes = 4 * 3 * 2 * P * R;
         }
-    CHECK(memcmp(out, chunk, (size_t)(L * 2 * T * R)) == 0, "offload round trip");
-    free(img);
-    CHECK(kvio_pool_destroy(pool) == KVIO_OK, "destroy");
+        d.num_layers = L;
+        d.num_kv_heads = H;
+        d.head_dim = D;
+        d.elem_bytes = 2;
+        d.page_size = P;
+        d.num_slots = S;
+        d.k_layers = kl;
+        d.v_layers = vl;
+        CHECK(kvio_pool_create(&d, &pool) == KVIO_OK, "pool create: %s", kvio_last_error());
+        span.host = chunk;
+        span.host_tokens = T;
+        span.num_tokens = T;
+        span.page_idx = pidx_dev;
+        CHECK(kvio_load(pool, &span, 1, 0, L, NULL) == KVIO_OK, "load (mode %d): %s", mode, kvio_last_error());
+        span.host = out;
+        CHECK(kvio_offload(pool, &span, 1, 0, L, NULL) == KVIO_OK, "offload: %s", kvio_last_error());
+        CHECK(kvio_check(pool) == KVIO_OK, "check: %s", kvio_last_error());
+        img = (uint8_t *)malloc((size_t)(2 * L * S * R));
+        CHECK(img != NULL, "malloc");
+        CHECK(hipMemcpy(img, pool_dev, (size_t)(2 * L * S * R), hipMemcpyDeviceToHost) == hipSuccess, "readback");
+        /* every moved row, by the definition; every other row still 0x5A */
+        for (l = 0; l < L; ++l)
+            for (kv = 0; kv < 2; ++kv) {
+                const uint8_t *plane = img + (int64_t)(kv * L + l) * S * R;
+                char *used = (char *)calloc(S, 1);
+                for (t = 0; t < T; ++t) {
+                    const int64_t slot = (int64_t)pidx[t / P] * P + t % P;
+                    const uint8_t *src = chunk + ((int64_t)(l * 2 + kv) * T + t) * R;
+                    used[slot] = 1;
+                    CHECK(memcmp(plane + slot * R, src, (size_t)R) == 0, "row l=%d kv=%d t=%lld", l, kv, (long long)t);
+                }
+                for (t = 0; t < S; ++t)
+                    if (!used[t])
+                        for (i = 0; i < R; ++i) CHECK(plane[t * R + i] == 0x5A, "untouched slot %lld", (long long)t);
+                free(used);
+            }
+        CHECK(memcmp(out, chunk, (size_t)(L * 2 * T * R)) == 0, "offload round trip (mode %d)", mode);
+        free(img);
+        CHECK(kvio_pool_destroy(pool) == KVIO_OK, "destroy");
+    }
     kvio_host_free(chunk);
     kvio_host_free(out);
     (void)hipFree(pool_dev);
