@@ -1,0 +1,76 @@
+"""Host-side helpers of bench.py (no GPU): the roofline block, the counter
+summary lookup keyed to the kernel sources, and the batch-formation drain
+model's accounting."""
+import hashlib
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_roofline_block():
+    r = bench.roofline("k", 57.6, 57.3, traffic=None, algorithmic_bytes_per_launch=4 << 30)
+    assert r["peak"] == 64.0 and r["unit"] == "GB/s" and r["bound"] == "host_link"
+    assert r["frac"] == round(57.6 / 64.0, 4)
+    assert r["frac_of_measured_peak"] == round(57.6 / 57.3, 4)
+    assert r["hbm"]["peak"] == 8000.0 and r["algorithmic_bytes_per_launch"] == 4 << 30
+    b = bench.roofline("k", 100.0, 97.3, directions=2)
+    assert b["peak"] == 128.0 and "both directions" in b["bound"]
+    assert bench.roofline("k", 50.0, None)["frac_of_measured_peak"] is None
+
+
+def test_measured_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_2508_18572_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    (csrc / "kvio_kernels.hip").write_bytes(b"kernel")
+    (csrc / "kvio_internal.h").write_bytes(b"header")
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    hashes = " ".join(hashlib.sha256(x).hexdigest() for x in (b"kernel", b"header"))
+    (prof / "kvio_copy_kernel__llama8b_p1_32k.counters.txt").write_text(
+        f"# c\nkernel_sources_sha256: {hashes}\nload_fetch_kib: 100.0\nload_write_kib: 200.0\n"
+        "fetch_scale: 2.0\nwrite_scale: 1.0\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    t = bench.measured_traffic(2, True)
+    assert t["fetch_bytes"] == 200 * 1024 and t["write_bytes"] == 200 * 1024 and t["bytes"] == 400 * 1024
+    assert bench.measured_traffic(2, False) is None           # another launch shape
+    assert bench.measured_traffic(1, True) is None            # another workload
+    (csrc / "kvio_kernels.hip").write_bytes(b"changed")
+    assert bench.measured_traffic(2, True) is None            # kernel changed since the counters
+
+
+def test_committed_counters_match_the_kernel_sources():
+    """Whether the committed counter summary names the current kernel sources
+    (then the bench reports measured traffic; otherwise traffic is null until
+    the counters are re-taken)."""
+    if bench.measured_traffic(2, True) is None:
+        pytest.skip("the committed counters were taken on other kernel sources: re-take them")
+
+
+class _FakeKv:
+    """Algorithm 1 stand-in for the drain model: FIFO batches of two."""
+
+    @staticmethod
+    def kvio_schedule_round(q, max_tokens, max_requests, ratio):
+        take = list(range(min(2, len(q))))
+        return take, list(range(len(take), len(q)))
+
+
+def test_drain_model_counts_a_shared_context_once():
+    q = [(1000, 10, 7, 0), (1000, 10, 7, 0), (0, 50, None, 0)]
+    r = bench.drain_queue(_FakeKv, q, 100.0, load_tok_s=1000.0, prefill_tok_s=10.0)
+    # batch 1: context 7 once -> load 1 s, compute 2 s -> 2 s; batch 2: compute 5 s
+    assert r["drain_s"] == pytest.approx(7.0) and r["batches"] == 2 and r["loading_bound_batches"] == 0
+    assert r["mean_completion_s"] == pytest.approx((2 + 2 + 7) / 3, abs=1e-3)
+
+
+def test_synthetic_queue_is_seeded():
+    a, b = bench.synthetic_queue(200, 5), bench.synthetic_queue(200, 5, bursty=True)
+    assert a == bench.synthetic_queue(200, 5) and len(a) == len(b) == 200
+    cached = [r for r in a if r[2] is not None]
+    assert cached and all(8192 <= r[0] < 131072 and 64 <= r[1] < 512 for r in cached)
+    assert all(r[0] == 0 and 1024 <= r[1] < 8192 for r in a if r[2] is None)
