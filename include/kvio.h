@@ -37,11 +37,13 @@
  *     reported synchronously and enqueue nothing.
  *   - The caller owns every buffer: pools, host chunks, page tables.  The
  *     library owns only the pool handle (a device copy of the layer-pointer
- *     table and a device error record).
+ *     table, a device error record and, for directions launched with
+ *     KVIO_LAUNCH_STAGED, HBM staging slots with a side stream and events).
  *   - A pool handle is immutable after creation and may be used from several
  *     threads and streams at once.  Transfers that run concurrently must write
- *     disjoint bytes; a load whose page tables name one pool slot twice leaves
- *     that slot holding one of the rows (unspecified which).
+ *     disjoint bytes (and staged transfers of one direction must not overlap);
+ *     a load whose page tables name one pool slot twice leaves that slot
+ *     holding one of the rows (unspecified which).
  *   - Page indices are range-checked on the device at no measurable cost: a
  *     row whose page lies outside [0, S / P) is skipped, never dereferenced,
  *     and the first such (span, context page) is recorded for kvio_check().
