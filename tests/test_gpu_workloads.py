@@ -70,7 +70,7 @@ def test_workload1_tiny_pool_exact(kv):
         pool.close()
 
 
-def single_context_workload(kv, k, io_stream, layerwise=False):
+def single_context_workload(kv, k, io_stream, layerwise=False, staged=False):
     import torch
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -83,7 +83,8 @@ def single_context_workload(kv, k, io_stream, layerwise=False):
     pt = torch.from_numpy(pages).cuda()
     with kv.HostBuffer(nbytes) as hb, kv.HostBuffer(nbytes) as ob:
         W.fill_cuda(hb.ptr, nbytes, W.data_seed(k), shp)
-        pool = kv.KVPool(pool_t, P)
+        launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None
+        pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
         span = [(hb.ptr, T, T, pt.data_ptr())]
         if layerwise:
             side = io_stream
@@ -114,6 +115,16 @@ def test_workload2_llama8b_page1(kv, io_stream):
 
 def test_workload3_70b_layerwise(kv, io_stream):
     single_context_workload(kv, 3, io_stream, layerwise=True)
+
+
+def test_workload2_staged(kv, io_stream):
+    """Staged transfers at full size: a 4 GiB context, whole layers per slot."""
+    single_context_workload(kv, 2, io_stream, staged=True)
+
+
+def test_workload3_staged_layerwise(kv, io_stream):
+    """Staged layer-wise loads of the 70B context (one slot per layer)."""
+    single_context_workload(kv, 3, io_stream, layerwise=True, staged=True)
 
 
 def test_workload4_batched_churned(kv):
@@ -174,9 +185,12 @@ def test_workload4_batched_churned(kv):
     pool.close()
 
 
-def test_workload5_1m_with_concurrent_offload(kv, io_stream):
+@pytest.mark.parametrize("staged", [False, True], ids=["kernel", "staged_load"])
+def test_workload5_1m_with_concurrent_offload(kv, io_stream, staged):
     """1M-token load at page size 1 on one stream while 16K other slots are
-    offloaded repeatedly to a separate host chunk on a second stream."""
+    offloaded repeatedly to a separate host chunk on a second stream (the
+    load through the kernels, or staged through HBM slots: 2 GiB per layer,
+    so spans split across slots)."""
     import torch
     k = 5
     wl = W.WORKLOADS[k]
@@ -189,7 +203,7 @@ def test_workload5_1m_with_concurrent_offload(kv, io_stream):
     load_slots, off_slots = both[:T].copy(), both[T:].copy()
     nb, nbo = L * 2 * T * R, L * 2 * TO * R
     pool_t = new_pool(L, S, H, D, torch.bfloat16)
-    pool = kv.KVPool(pool_t, P)
+    pool = kv.KVPool(pool_t, P, load_launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None)
     pl, po = torch.from_numpy(load_slots).cuda(), torch.from_numpy(off_slots).cuda()
     with kv.HostBuffer(nb) as hb, kv.HostBuffer(nbo) as src_o, kv.HostBuffer(nbo) as dst_o:
         W.fill_cuda(hb.ptr, nb, W.data_seed(k), shp)
