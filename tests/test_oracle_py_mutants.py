@@ -76,6 +76,7 @@ def test_pins_catch_mutant(tmp_path, module, name, old, new):
     tests = tmp_path / "tests"
     tests.mkdir()
     (tests / "conftest.py").write_text(CONFTEST)
+    shutil.copytree(os.path.join(ROOT, "tests", "golden"), tests / "golden")
     shutil.copy(os.path.join(ROOT, "tests", PINS[module]), tests / PINS[module])
     env = dict(os.environ)
     env.pop("PYTHONPATH", None)
@@ -92,6 +93,7 @@ def test_unmutated_copy_passes(tmp_path):
     tests = tmp_path / "tests"
     tests.mkdir()
     (tests / "conftest.py").write_text(CONFTEST)
+    shutil.copytree(os.path.join(ROOT, "tests", "golden"), tests / "golden")
     for f in PINS.values():
         shutil.copy(os.path.join(ROOT, "tests", f), tests / f)
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-p", "no:cacheprovider", str(tests)],

@@ -6,7 +6,9 @@ Algorithm 1 forms (C, F) so C's load overlaps F's compute, and D0 with D1 —
 which share one context — form a bundle-hit batch next.  The numbers below
 are chosen so that exactly those decisions follow from a ratio of 100.
 """
+import json
 import math
+import os
 
 import pytest
 
@@ -28,6 +30,32 @@ def fig7():
     D1 = Request(2, 60_000, 200, context=7)
     F = Request(3, 0, 2_000)
     return [C, D0, D1, F]
+
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "fig7_batch_formation.json")
+
+
+def golden_fig7():
+    g = json.load(open(GOLDEN))
+    reqs = [Request(i, r["load_tokens"], r["compute_tokens"], r["context"]) for i, r in enumerate(g["requests"])]
+    names = [r["name"] for r in g["requests"]]
+    return g, reqs, names
+
+
+def test_figure7_golden_rounds():
+    """The stored Figure 7 fixture, round by round, through schedule_round."""
+    g, reqs, names = golden_fig7()
+    pol = g["policy"]
+    by_name = dict(zip(names, reqs))
+    queue = reqs
+    for rnd in g["rounds"]:
+        batch, nxt = schedule_round(queue, pol["max_tokens"], pol["max_requests"], pol["loading_bound_ratio"],
+                                    pol["delay_hit_threshold"])
+        assert [names[i] for i in batch] == rnd["batch"]
+        assert [names[i] for i in nxt] == rnd["next_queue"]
+        queue = [by_name[n] for n in rnd["next_queue"]]
+    fifo, _ = batch_formation(reqs, pol["max_tokens"], pol["max_requests"], ratio=INF)
+    assert [names[i] for i in fifo] == g["fifo_first_batch"]
 
 
 def test_figure7_worked_example():

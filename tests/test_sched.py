@@ -31,6 +31,24 @@ def test_figure7(kv):
     assert kv.kvio_schedule_round(reqs, 8_000, 2) == ([0, 3], [1, 2])
 
 
+def test_figure7_golden(kv):
+    """The stored Figure 7 fixture through the library, round by round."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                    "fig7_batch_formation.json")))
+    names = [r["name"] for r in g["requests"]]
+    reqs = {r["name"]: (r["load_tokens"], r["compute_tokens"], -1 if r["context"] is None else r["context"], 0)
+            for r in g["requests"]}
+    pol = g["policy"]
+    queue = names
+    for rnd in g["rounds"]:
+        batch, nxt = kv.kvio_schedule_round([reqs[n] for n in queue], pol["max_tokens"], pol["max_requests"],
+                                            pol["loading_bound_ratio"], pol["delay_hit_threshold"])
+        assert [queue[i] for i in batch] == rnd["batch"] and [queue[i] for i in nxt] == rnd["next_queue"]
+        queue = rnd["next_queue"]
+
+
 def test_edges(kv):
     assert run_both(kv, [], 100, 4) == ([], [])
     assert run_both(kv, [(0, 10, -1, 500)] * 3, 100, 4) == ([], [0, 1, 2])       # all deferred
