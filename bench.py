@@ -704,6 +704,8 @@ def run_interference(args, torch, kv, W):
               (64, 256), (128, 256), (32, 64), (64, 64), (128, 64), (256, 64), (64, 128), (128, 128),
               ("staged", None)]
     rows = []
+    for fn in corunners.values():               # warm the clocks before the first baseline
+        alone(fn, 50)
     base = {name: alone(fn) for name, fn in corunners.items()}
     log(f"co-runners alone: " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
     for wg, th in quotas:
@@ -737,11 +739,19 @@ def run_interference(args, torch, kv, W):
             inside = [x.elapsed_time(y) for x, y in marks
                       if start.elapsed_time(x) >= t0 and start.elapsed_time(y) <= t1]
             row[f"load_gbps_with_{name}"] = round(nb / ((t1 - t0) * 1e-3) / GB, 3)
-            row[f"{name}_slowdown"] = round(statistics.median(inside) / base[name], 4) if inside else None
+            row[f"{name}_ms_corun"] = round(statistics.median(inside), 4) if inside else None
         pool.close()
         rows.append(row)
-        log(f"quota {wg!s:>6} x {th!s:>4}: " + ", ".join(f"{k2} {v}" for k2, v in row.items()
-                                                    if k2 not in ("workgroups", "threads")))
+    # the baseline: the faster of the co-runner alone before and after the sweep
+    after = {name: alone(fn) for name, fn in corunners.items()}
+    base = {n: min(base[n], after[n]) for n in base}
+    log(f"co-runners alone (best of before / after the sweep): " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
+    for row in rows:
+        for name in corunners:
+            t = row[f"{name}_ms_corun"]
+            row[f"{name}_slowdown"] = round(t / base[name], 4) if t else None
+        log(f"quota {row['workgroups']!s:>6} x {row['threads']!s:>4}: " + ", ".join(
+            f"{k2} {v}" for k2, v in row.items() if k2 not in ("workgroups", "threads")))
     res = base_result(args, max(r["load_gbps_alone"] for r in rows), 0.0,
                       "interference sweep on config2: Llama-3.1-8B KV, page size 1, 32K-token load",
                       {"corunners": {"prefill_gemm": [8192, 4096, 14336], "decode_hbm_bytes": 8 << 30},
