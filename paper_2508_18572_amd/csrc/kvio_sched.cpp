@@ -13,9 +13,12 @@
 
 namespace {
 
+// Token sums are kept in 128 bits: n requests of up to 2^63 tokens each
+// cannot overflow them, and the loading-bound test converts them to double
+// (rounding to nearest) as the definition does.
 struct Batch {
-    int64_t load = 0;
-    int64_t compute = 0;
+    __int128 load = 0;
+    __int128 compute = 0;
     int32_t count = 0;
     std::unordered_set<int64_t> contexts;
 };
@@ -61,8 +64,8 @@ extern "C" kvio_status kvio_schedule_round(const kvio_request *queue, int32_t n,
     };
     auto is_full = [&]() { return B.compute >= policy->max_tokens || B.count >= policy->max_requests; };
     auto loading_bound = [&](int32_t i) {
-        const int64_t load = B.load + (is_bundle_hit(i) ? 0 : queue[i].load_tokens);
-        const int64_t compute = B.compute + queue[i].compute_tokens;
+        const __int128 load = B.load + (is_bundle_hit(i) ? 0 : queue[i].load_tokens);
+        const __int128 compute = B.compute + queue[i].compute_tokens;
         return double(load) > ratio * double(compute);
     };
     auto add = [&](int32_t i) {
