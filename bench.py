@@ -216,6 +216,17 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
     return res
 
 
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), else the machine type."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.machine() or "host CPU"
+
+
 def cpu_baseline(pool_rows, row_bytes, host, host_tokens, num_tokens, pages, page_size, L, seconds):
     """The CPU oracle (single thread) loading then offloading the same context,
     one (layer, K|V) slab at a time into a host image of one pool slab, until
@@ -351,7 +362,7 @@ def run_layerwise(args, torch, kv, W):
     shp = wl.shape
     L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
     R = shp.row_bytes
-    log(f"config 3: {wl.description}; L={L} P={P} S={S} T={T}")
+    log(f"{wl.description}; L={L} P={P} S={S} T={T}")
     pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
     pages = W.random_pages(np.random.default_rng(W.placement_seed(k)), S // P, -(-T // P))
     pidx = torch.from_numpy(pages).cuda()
@@ -433,7 +444,7 @@ def run_layerwise(args, torch, kv, W):
     log(f"load alone {tl:.2f} ms ({load_gbps:.2f} GB/s), GEMMs alone {tg:.2f} ms ({gemm_tflops:.0f} TFLOP/s), "
         f"both {tb:.2f} ms; load co-run {load_gbps_co:.2f} GB/s; GEMM time co-run {tg_co:.2f} ms; "
         f"overlap efficiency {overlap:.3f}")
-    res = base_result(args, load_gbps_co, tb, f"config3: {wl.description}",
+    res = base_result(args, load_gbps_co, tb, wl.description,
                       {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "tokens": T,
                        "payload_bytes": nbytes, "bytes_per_layer_launch": per_layer,
                        "gemm_per_layer": [M, N, K], "step": "80 x (kvio_load_layer on a side stream; "
@@ -478,7 +489,7 @@ def run_batched(args, torch, kv, W):
         acc += b
     waves.append(cur)
     total = sum(sizes)
-    log(f"config 4: {sum(hit)} tokens, {total / 2**30:.1f} GiB, pool {S} slots, {len(waves)} waves, "
+    log(f"batched partial hits: {sum(hit)} tokens, {total / 2**30:.1f} GiB, pool {S} slots, {len(waves)} waves, "
         f"mean page-run length {req.mean_run_length:.2f}")
     pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
     lc = launch_from(args, kv)
@@ -514,7 +525,7 @@ def run_batched(args, torch, kv, W):
     tload, toff = sum(load_ms), sum(off_ms)
     load_gbps, off_gbps = total / (tload * 1e-3) / GB, total / (toff * 1e-3) / GB
     log(f"batched load {load_gbps:.2f} GB/s, offload {off_gbps:.2f} GB/s over {len(waves)} waves")
-    res = base_result(args, load_gbps, tload, "config4: batched partial hits of the Llama-3.1-8B KV shape, "
+    res = base_result(args, load_gbps, tload, "batched partial hits of the Llama-3.1-8B KV shape, "
                       "page size 16, churned pool",
                       {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "requests": len(hit),
                        "tokens": sum(hit), "payload_bytes": total, "waves": len(waves),
@@ -617,7 +628,7 @@ def run_bidirectional(args, torch, kv, W):
     log(f"load alone {nb / (t_load_alone * 1e-3) / GB:.2f} GB/s, offload alone {nbo / (t_off_alone * 1e-3) / GB:.2f} "
         f"GB/s; concurrent: load {load_gbps:.2f} GB/s, offload {off_gbps:.2f} GB/s ({n_in} runs), "
         f"combined {bidir:.2f} GB/s")
-    res = base_result(args, bidir, t_load, f"config5: {wl.description}",
+    res = base_result(args, bidir, t_load, wl.description,
                       {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "tokens": T,
                        "offload_tokens_per_run": TO, "payload_bytes_load": nb, "payload_bytes_per_offload": nbo,
                        "background_offload_launch": {"workgroups": bg[0], "threads": bg[1], "tile_kib": bg[2]},
@@ -753,7 +764,7 @@ def run_interference(args, torch, kv, W):
         log(f"quota {row['workgroups']!s:>6} x {row['threads']!s:>4}: " + ", ".join(
             f"{k2} {v}" for k2, v in row.items() if k2 not in ("workgroups", "threads")))
     res = base_result(args, max(r["load_gbps_alone"] for r in rows), 0.0,
-                      "interference sweep on config2: Llama-3.1-8B KV, page size 1, 32K-token load",
+                      "interference sweep: Llama-3.1-8B KV, page size 1, 32K-token load into random slots",
                       {"corunners": {"prefill_gemm": [8192, 4096, 14336], "decode_hbm_bytes": 8 << 30},
                        "corunner_ms_alone": {n: round(t, 4) for n, t in base.items()}})
     res["sweep"] = rows
@@ -1194,7 +1205,7 @@ def run_single(args, torch, kv, W, k):
     L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
     R = shp.row_bytes
     dtype = torch.float16 if shp.dtype == "fp16" else torch.bfloat16
-    log(f"config {k}: {wl.description}; L={L} H={H} D={D} P={P} S={S} T={T} R={R}")
+    log(f"{wl.description}; L={L} H={H} D={D} P={P} S={S} T={T} R={R}")
 
     # ---- inputs, resident before timing -------------------------------------------------
     pool_t = torch.empty((2, L, S, H, D), dtype=dtype, device="cuda")
@@ -1284,7 +1295,7 @@ def run_single(args, torch, kv, W, k):
         cpu = {"value": nbytes / el / GB, "unit": "GB/s", "cores": 1, "kind": "oracle",
                "sample": f"{passes} pass(es) of load+offload of the whole {T}-token context, one "
                          f"(layer, K|V) slab at a time into a {S}-row host slab image, "
-                         f"{el:.1f} s on {platform.processor() or 'host CPU'} "
+                         f"{el:.1f} s on {cpu_model()} "
                          f"({len(os.sched_getaffinity(0))} cores available, 1 used)"}
         log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
 
@@ -1313,7 +1324,7 @@ def run_single(args, torch, kv, W, k):
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
-        "config": {"workload": f"config{k}: {wl.description}", "kv_shape": shp.name, "layers": L,
+        "config": {"workload": wl.description, "kv_shape": shp.name, "layers": L,
                    "kv_heads": H, "head_dim": D, "kv_dtype": shp.dtype, "page_size": P, "pool_slots": S,
                    "tokens": T, "payload_bytes_per_direction": payload,
                    "step": "kvio_load (all layers) + kvio_offload (all layers)",

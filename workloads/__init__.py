@@ -70,7 +70,8 @@ class Workload:
 
 WORKLOADS = {
     1: Workload(1, TINY, 16, 4096, 1024,
-                "tiny pool, 1024-token context into 64 random pages, round trip"),
+                "tiny pool (2 layers, 4 KV heads x 64 dims, fp16, 4096 slots), page size 16, "
+                "1024-token context into 64 random pages, round trip"),
     2: Workload(2, LLAMA8B, 1, 500_000, 32 * KiB,
                 "Llama-3.1-8B KV, page size 1, 32K-token prefix into random free slots"),
     3: Workload(3, GQA70B, 16, 131_072, 64 * KiB,
