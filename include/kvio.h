@@ -112,7 +112,10 @@ typedef enum kvio_status {
  * the work already on the call's stream, and the call's stream has passed
  * all of its work (a load: its last scatter) when the call completes in
  * stream order.  The launch fields shape the scatter / gather kernel (defaults
- * 1024 x 256, 16 KiB steps).  Calls in one direction on one handle share that
+ * 1024 x 256, 16 KiB steps).  A call that moves less than 64 MiB in total
+ * (or less than one slot, if slots are smaller) runs on the kernel path
+ * (default shape) instead: staging cannot amortise its per-copy and hand-over
+ * costs on small transfers.  Calls in one direction on one handle share that
  * direction's staging, so they must not overlap (same stream, or ordered by
  * events).  An out-of-range page is still skipped and reported by kvio_check,
  * but a staged offload then leaves unspecified bytes in the host rows of its
