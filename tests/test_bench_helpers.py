@@ -74,3 +74,12 @@ def test_synthetic_queue_is_seeded():
     cached = [r for r in a if r[2] is not None]
     assert cached and all(8192 <= r[0] < 131072 and 64 <= r[1] < 512 for r in cached)
     assert all(r[0] == 0 and 1024 <= r[1] < 8192 for r in a if r[2] is None)
+
+
+def test_more_than_one_gpu_is_refused():
+    import json
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
