@@ -69,6 +69,8 @@ def parse():
     ap.add_argument("--staged", action="store_true",
                     help="copy engine through an HBM staging buffer + scatter/gather kernel (KVIO_LAUNCH_STAGED)")
     ap.add_argument("--staging-mib", type=int, default=0, help="staging per direction (4 slots); 0 = default")
+    ap.add_argument("--gemm-m", type=int, default=4096,
+                    help="layer-wise workload: rows of the per-layer GEMM (4096 = load-bound; 65536 = compute-bound)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
     ap.add_argument("--no-peak", action="store_true")
@@ -355,8 +357,9 @@ def layout_from(args, kv):
 def run_layerwise(args, torch, kv, W):
     """70B GQA KV at page size 16: a 64K-token context loaded layer by layer on a
     side stream (kvio_load_layer, one event per layer) while a compute stream
-    runs one bf16 GEMM (4096 x 8192 x 8192) per layer, each GEMM waiting on its
-    layer's event (layer-wise overlap, Strata Sec. 4.1 / Sec. 4.2.1)."""
+    runs one bf16 GEMM (M x 8192 x 8192, M = 4096 by default: load-bound) per
+    layer, each GEMM waiting on its layer's event (layer-wise overlap, Strata
+    Sec. 4.1 / Sec. 4.2.1)."""
     k = 3
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -374,7 +377,7 @@ def run_layerwise(args, torch, kv, W):
                      staging_bytes=args.staging_mib << 20)
     span = [(host.ptr, T, T, pidx.data_ptr())]
     side, comp = io_stream(torch, kv), torch.cuda.Stream()
-    M, N, K = 4096, 8192, 8192
+    M, N, K = args.gemm_m, 8192, 8192
     g = torch.Generator(device="cuda").manual_seed(W.data_seed(k))
     A = torch.randn(M, K, device="cuda", dtype=torch.bfloat16, generator=g)
     B = torch.randn(K, N, device="cuda", dtype=torch.bfloat16, generator=g)
