@@ -253,6 +253,43 @@ def cpu_baseline(pool_rows, row_bytes, host, host_tokens, num_tokens, pages, pag
     return nbytes, el, passes
 
 
+def cpu_baseline_all_cores(pool_rows, row_bytes, host, host_tokens, num_tokens, pages, page_size, L, seconds,
+                           threads):
+    """The same CPU oracle, unchanged, on `threads` host threads at once: each
+    thread loads then offloads its own share of the (layer, K|V) slabs into a
+    slab image of its own (the oracle's C calls run without the interpreter
+    lock), until `seconds` have passed."""
+    import threading
+
+    import oracle
+    h = host.reshape(L, 2, host_tokens * row_bytes)
+    planes = [(l, kvi) for l in range(L) for kvi in range(2)]
+    done = [0] * threads
+    stop = threading.Event()
+
+    def work(w):
+        slab = np.zeros((pool_rows, row_bytes), np.uint8)
+        out = np.zeros(num_tokens * row_bytes, np.uint8)
+        i = w
+        while not stop.is_set():
+            l, kvi = planes[i % len(planes)]
+            oracle.load_slab(slab, page_size, h[l, kvi], num_tokens, pages)
+            oracle.offload_slab(slab, page_size, out, num_tokens, pages)
+            done[w] += 1
+            i += threads
+
+    workers = [threading.Thread(target=work, args=(w,)) for w in range(threads)]
+    t0 = time.perf_counter()
+    for t in workers:
+        t.start()
+    time.sleep(seconds)
+    stop.set()
+    for t in workers:
+        t.join()
+    el = time.perf_counter() - t0
+    return sum(done) * 2 * num_tokens * row_bytes, el, sum(done)
+
+
 def steady_state(torch, kv, pool, span, host, stream, payload, reps):
     """Small-context latency: one load alone (host launch to completion, and
     GPU time), then `reps` back-to-back loads; the same for a contiguous
@@ -1292,7 +1329,7 @@ def run_single(args, torch, kv, W, k):
         log(f"naive per-page memcpy: {calls} calls, {naive['gbps']:.2f} GB/s")
 
     # ---- CPU oracle baseline --------------------------------------------------------------
-    cpu = None
+    cpu = cpu_all = None
     if not args.no_cpu_baseline and args.host_layout == "token":
         nbytes, el, passes = cpu_baseline(S, R, host.array, T, T, pages, P, L, args.cpu_seconds)
         cpu = {"value": nbytes / el / GB, "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -1301,6 +1338,12 @@ def run_single(args, torch, kv, W, k):
                          f"{el:.1f} s on {cpu_model()} "
                          f"({len(os.sched_getaffinity(0))} cores available, 1 used)"}
         log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
+        nthreads = min(len(os.sched_getaffinity(0)), 16)
+        nbytes, el, slabs = cpu_baseline_all_cores(S, R, host.array, T, T, pages, P, L, args.cpu_seconds, nthreads)
+        cpu_all = {"value": nbytes / el / GB, "unit": "GB/s", "cores": nthreads, "kind": "oracle",
+                   "sample": f"{slabs} (layer, K|V) slab load+offloads of the same context on {nthreads} threads, "
+                             f"each into its own {S}-row slab image, {el:.1f} s on {cpu_model()}"}
+        log(f"cpu oracle: {cpu_all['value']:.2f} GB/s on {nthreads} threads")
 
     steady = None
     if k == 1:
@@ -1350,6 +1393,7 @@ def run_single(args, torch, kv, W, k):
                              algorithmic_bytes_per_launch=payload, algorithmic_traffic_per_launch=2 * payload),
         "naive": naive,
         "cpu_baseline": cpu,
+        "cpu_baseline_all_cores": cpu_all,
     }
     if steady:
         result["steady_state"] = steady
