@@ -34,7 +34,10 @@
  *     crosses the ABI.  On error kvio_last_error() holds a thread-local text.
  *   - Transfers are asynchronous on the given stream (NULL = the default
  *     stream); completion follows stream order.  Validation errors are
- *     reported synchronously and enqueue nothing.
+ *     reported synchronously and enqueue nothing.  The transfer calls enqueue
+ *     no memset and allocate nothing, so they can be captured into a HIP
+ *     graph (a staged call forks its side stream from the captured stream and
+ *     joins it back through events).
  *   - The caller owns every buffer: pools, host chunks, page tables.  The
  *     library owns only the pool handle (a device copy of the layer-pointer
  *     table, a device error record and, for directions launched with
