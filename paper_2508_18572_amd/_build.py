@@ -8,7 +8,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvio.so")
 SOURCES = [os.path.join(CSRC, "kvio_kernels.hip"), os.path.join(CSRC, "kvio_api.cpp"),
-           os.path.join(CSRC, "kvio_sched.cpp"), os.path.join(CSRC, "kvio_disk.cpp")]
+           os.path.join(CSRC, "kvio_sched.cpp"), os.path.join(CSRC, "kvio_disk.cpp"),
+           os.path.join(CSRC, "kvio_staged.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
