@@ -82,6 +82,9 @@ def parse():
     ap.add_argument("--page-sweep", action="store_true",
                     help="Llama-3.1-8B KV: kvio vs one hipMemcpyAsync per page segment over page sizes "
                          "1..256 (32K tokens), plus 8192 tokens at page size 32")
+    ap.add_argument("--row-sweep", action="store_true",
+                    help="GB/s against the token row size (KV heads x 128 dims x bf16 from 256 B to 8 KiB), "
+                         "page size 1 and 16: the per-rank shapes of tensor-parallel serving")
     ap.add_argument("--schedule", action="store_true",
                     help="cache-aware batch formation: scheduling cost per round, and FIFO vs Algorithm 1 "
                          "on a synthetic queue under a cost model built from measured load and GEMM rates")
@@ -812,6 +815,72 @@ def run_interference(args, torch, kv, W):
     print(json.dumps(res), flush=True)
 
 
+def run_row_sweep(args, torch, kv, W):
+    """GB/s against the token row size R = H x 128 x 2 bytes for H = 1 .. 32 KV
+    heads (256 B .. 8 KiB; a 70B model's 8 KV heads split over 4 or 8
+    tensor-parallel ranks gives R = 512 B or 256 B per rank), 80 layers, 2 GiB
+    per direction per case, at page size 1 (random slots) and 16 (random
+    pages); default launch shapes, HIP events on the transfer stream, median
+    of 5 after a warm-up, round trip checked."""
+    L, D = 80, 128
+    nb = 2 << 30
+    stream = io_stream(torch, kv)
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    host, out = kv.HostBuffer(nb), kv.HostBuffer(nb)
+    W.fill_cuda(host.ptr, nb, W.data_seed(3), W.GQA70B)
+    rows = []
+    try:
+        for H in (1, 2, 4, 8, 16, 32):
+            R = H * D * 2
+            T = nb // (L * 2 * R)
+            for P in (1, 16):
+                S = -(-2 * T // P) * P
+                pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+                rng = np.random.default_rng(600 + H * 7 + P)
+                pages = W.random_slots(rng, S, T) if P == 1 else W.random_pages(rng, S // P, -(-T // P))
+                pidx = torch.from_numpy(pages).cuda()
+                pool = kv.KVPool(pool_t, P)
+                span_in, span_out = [(host.ptr, T, T, pidx.data_ptr())], [(out.ptr, T, T, pidx.data_ptr())]
+                row = {"kv_heads": H, "row_bytes": R, "page_size": P, "tokens": T, "bytes": L * 2 * T * R}
+                for name, fn in (("load", lambda: pool.load(span_in, stream=stream)),
+                                 ("offload", lambda: pool.offload(span_out, stream=stream))):
+                    fn()
+                    torch.cuda.synchronize()
+                    t = Timer(torch, stream)
+                    for _ in range(5):
+                        e = t.start()
+                        fn()
+                        t.stop(e)
+                    torch.cuda.synchronize()
+                    row[f"{name}_gbps"] = round(row["bytes"] / (statistics.median(t.ms()) * 1e-3) / GB, 3)
+                pool.check()
+                if not memequal_np(out.array, host.array, row["bytes"]):
+                    raise SystemExit(f"round trip differs at H={H}, P={P}")
+                if peak:
+                    row["load_frac_of_h2d_peak"] = round(row["load_gbps"] / peak["h2d"], 4)
+                    row["offload_frac_of_d2h_peak"] = round(row["offload_gbps"] / peak["d2h"], 4)
+                log(", ".join(f"{k2} {v}" for k2, v in row.items()))
+                rows.append(row)
+                pool.close()
+                del pool_t
+    finally:
+        host.free()
+        out.free()
+    res = base_result(args, min(r["load_gbps"] for r in rows), 0.0,
+                      "row-size sweep: 80 layers, 1..32 KV heads x 128 dims bf16, 2 GiB per direction, "
+                      "page sizes 1 and 16", {})
+    res["metric"] = "kvio load / offload GB/s against the token row size"
+    res["host_link_peak"] = {k2: round(v, 3) for k2, v in peak.items()} if peak else None
+    res["sweep"] = rows
+    print(json.dumps(res), flush=True)
+
+
+def memequal_np(a, b, n):
+    """a[:n] == b[:n] for two large uint8 arrays, compared in 256 MiB pieces."""
+    step = 256 << 20
+    return all(np.array_equal(a[i:min(i + step, n)], b[i:min(i + step, n)]) for i in range(0, n, step))
+
+
 def run_page_sweep(args, torch, kv, W):
     """GB/s against page size (the synthetic analogue of Fig. 10's page-size
     axis) and the paper's own microbenchmark of Fig. 3 (8192 tokens at page
@@ -1228,6 +1297,8 @@ def main():
             run_disk(args, torch, kv, W)
         elif args.page_sweep:
             run_page_sweep(args, torch, kv, W)
+        elif args.row_sweep:
+            run_row_sweep(args, torch, kv, W)
         elif args.schedule:
             run_schedule(args, torch, kv, W)
         elif k in EXTRA_MODES:
