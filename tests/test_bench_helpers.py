@@ -83,3 +83,12 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
+
+
+def test_memequal_np_stops_at_n():
+    import numpy as np
+    a = np.zeros(3 << 20, np.uint8)
+    b = a.copy()
+    b[(2 << 20) + 5:] = 1
+    assert bench.memequal_np(a, b, (2 << 20) + 5)
+    assert not bench.memequal_np(a, b, (2 << 20) + 6)
