@@ -101,9 +101,9 @@ typedef enum kvio_status {
  * take the library defaults.  Results never depend on these. */
 #define KVIO_LAUNCH_CACHED 0x1     /* plain loads/stores instead of non-temporal ones */
 #define KVIO_LAUNCH_NO_LDS 0x2     /* head-major chunks: gather directly, no LDS staging */
-/* KVIO_LAUNCH_STAGED (token-major chunks only): instead of wavefronts reading
- * (writing) the pinned chunk across the host link, the copy engine moves the
- * chunk's contiguous (layer, K|V) token runs to (from) an HBM staging buffer
+/* KVIO_LAUNCH_STAGED (token-major and head-major chunks): instead of
+ * wavefronts reading (writing) the pinned chunk across the host link, the
+ * copy engine moves the chunk's contiguous runs to (from) an HBM staging buffer
  * of the pool handle with hipMemcpyAsync, and a kernel scatters (gathers) the
  * rows between the staging buffer and the paged pool -- the layout conversion
  * then runs at HBM speed on the whole chip for short bursts, and the long

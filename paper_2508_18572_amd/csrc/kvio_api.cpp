@@ -229,8 +229,8 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
     const bool staged[2] = {(d->load_launch.flags & KVIO_LAUNCH_STAGED) != 0,
                             (d->offload_launch.flags & KVIO_LAUNCH_STAGED) != 0};
     const int64_t stage_bytes = d->staging_bytes > 0 ? d->staging_bytes : kDefaultStagingBytes;
-    if ((staged[0] || staged[1]) && d->host_layout != KVIO_HOST_TOKEN_MAJOR)
-        return fail(KVIO_EINVAL, "kvio_pool_create: staged transfers take token-major host chunks");
+    if ((staged[0] || staged[1]) && d->host_layout == KVIO_HOST_PAGE_FIRST)
+        return fail(KVIO_EINVAL, "kvio_pool_create: staged transfers take token-major or head-major host chunks");
     const int64_t slot_bytes = stage_bytes / kStageSlots / 16 * 16;
     if ((staged[0] || staged[1]) && (d->staging_bytes < 0 || slot_bytes < 2 * int64_t(d->page_size) * R))
         return fail(KVIO_EINVAL, "kvio_pool_create: staging_bytes %lld must hold %d slots of at least one page "
@@ -412,8 +412,12 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
         int64_t bytes = 0;
         for (const Resolved &r : rs) bytes += r.num_tokens;
         bytes *= 2 * int64_t(l1 - l0) * p->row_bytes;
-        if (bytes >= std::min(kStagedMinBytes, p->slot_bytes))
-            return run_staged(p, rs, spans, n, l0, l1, stream, dir, resolve(lc, kvio::kDefaultStaged), fn);
+        if (bytes >= std::min(kStagedMinBytes, p->slot_bytes)) {
+            kvio::Shape shape = resolve(lc, kvio::kDefaultStaged);
+            if (p->host_layout == KVIO_HOST_HEAD_MAJOR && p->row_bytes > int64_t(shape.tile_kib) * 1024)
+                shape.head_major_lds = false;
+            return run_staged(p, rs, spans, n, l0, l1, stream, dir, shape, fn);
+        }
         lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
     }
     kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);

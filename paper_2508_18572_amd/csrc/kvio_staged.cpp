@@ -16,8 +16,10 @@ namespace kvio {
 
 // Staged transfer (KVIO_LAUNCH_STAGED).  Work is packed into staging slots as
 // units: span s, tokens [t0, t0 + n), layers [lb, lb + g) (shared by every
-// unit of a slot), laid out like a chunk of n tokens: row (l, kv, t) at
-// ((l - lb)*2 + kv)*n*R + (t - t0)*R from the unit.  When one layer of every
+// unit of a slot), laid out like a chunk of n tokens in the pool's host
+// layout: token-major row (l, kv, t) at ((l - lb)*2 + kv)*n*R + (t - t0)*R
+// from the unit; head-major segment (l, kv, h, t) at
+// (((l - lb)*2 + kv)*H + h)*n*De + (t - t0)*De.  When one layer of every
 // span fits a slot, units are whole spans over as many layers as fit, and a
 // span whose planes are contiguous (num_tokens == host_tokens) moves with one
 // copy; otherwise layer by layer, spans split into runs of whole pages.  The
@@ -58,12 +60,18 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
         };
         if (u.t0 == 0 && u.n == ht)           // whole planes: one contiguous run
             return one(host + int64_t(lb) * 2 * ht * R, slot + u.off, int64_t(g) * 2 * u.n * R);
+        // Token runs of one plane: contiguous rows (token-major), or one run
+        // of head segments per head (head-major: [H][host_tokens][De]).
+        const bool hm = p->host_layout == KVIO_HOST_HEAD_MAJOR;
+        const int64_t runs = hm ? p->num_heads : 1, run = hm ? p->seg_bytes : R;
         for (int32_t l = lb; l < lb + g; ++l)
-            for (int kv = 0; kv < 2; ++kv) {
-                hipError_t err = one(host + ((int64_t(l) * 2 + kv) * ht + u.t0) * R,
-                                     slot + u.off + ((int64_t(l - lb) * 2 + kv) * u.n) * R, u.n * R);
-                if (err != hipSuccess) return err;
-            }
+            for (int kv = 0; kv < 2; ++kv)
+                for (int64_t h = 0; h < runs; ++h) {
+                    hipError_t err = one(host + (((int64_t(l) * 2 + kv) * runs + h) * ht + u.t0) * run,
+                                         slot + u.off + (((int64_t(l - lb) * 2 + kv) * runs + h) * u.n) * run,
+                                         u.n * run);
+                    if (err != hipSuccess) return err;
+                }
         return hipSuccess;
     };
     auto flush = [&](int32_t lb, int32_t g) -> kvio_status {

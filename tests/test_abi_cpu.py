@@ -57,7 +57,7 @@ def test_host_side_validation_without_device():
         kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], offload_launch=kv.launch(tile_kib=5))
     assert e.value.status == kv.KVIO_EINVAL
     staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
-    with pytest.raises(kv.KvioError) as e:                      # staged: token-major chunks only
+    with pytest.raises(kv.KvioError) as e:                      # staged: not for page-first chunks
         kv.kvio_pool_create(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16], load_launch=staged,
                             host_layout=kv.KVIO_HOST_PAGE_FIRST)
     assert e.value.status == kv.KVIO_EINVAL and "token-major" in e.value.detail

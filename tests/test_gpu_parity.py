@@ -240,7 +240,7 @@ def test_staged_layer_call_and_errors(kv):
     with pytest.raises(kv.KvioError) as e:                  # slots smaller than one page of K and V
         kv.KVPool(pool_t, P, load_launch=staged, staging_bytes=4 * 2 * P * R - 16)
     assert e.value.status == kv.KVIO_EINVAL
-    with pytest.raises(kv.KvioError) as e:                  # staged transfers take token-major chunks only
+    with pytest.raises(kv.KvioError) as e:                  # staged transfers do not take page-first chunks
         kv.KVPool(pool_t, P, offload_launch=staged, host_layout=kv.KVIO_HOST_PAGE_FIRST)
     assert e.value.status == kv.KVIO_EINVAL
 

@@ -50,7 +50,7 @@ def draw_case(seed):
     flags = 0
     if rng.random() < 0.3:
         flags |= 0x1                                   # cached instead of non-temporal
-    staged = layout == 0 and rng.random() < 0.3
+    staged = layout in (0, 2) and rng.random() < 0.3
     if staged:
         flags |= 0x4
     if layout == 2 and rng.random() < 0.5:
