@@ -400,7 +400,12 @@ class HostBuffer:
 
 class KVPool:
     """A pool handle over a torch tensor shaped (2, L, S, H, D): K then V, each
-    layer a token-major (S, H, D) array of 16-bit elements."""
+    layer a token-major (S, H, D) array of 16-bit elements.
+
+    load_launch / offload_launch shape each direction (see launch(); a
+    KVIO_LAUNCH_STAGED flag stages that direction through HBM slots of
+    staging_bytes / 4 each, 0 = the library default); host_layout names the
+    layout of the host chunks this handle moves (KVIO_HOST_*)."""
 
     def __init__(self, pool: "torch.Tensor", page_size: int,
                  load_launch: Optional[kvio_launch] = None, offload_launch: Optional[kvio_launch] = None,
