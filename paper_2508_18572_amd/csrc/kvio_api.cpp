@@ -421,30 +421,15 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
         lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
     }
     kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);
-    const int64_t R = p->row_bytes;
     // LDS staging of a head-major tile needs the whole tile (>= one row) in the
     // wave's U KiB slice.
-    if (p->host_layout == KVIO_HOST_HEAD_MAJOR && R > int64_t(shape.tile_kib) * 1024) shape.head_major_lds = false;
-    const int rpt = kvio::rows_per_tile(R, shape.tile_kib);
+    if (p->host_layout == KVIO_HOST_HEAD_MAJOR && p->row_bytes > int64_t(shape.tile_kib) * 1024)
+        shape.head_major_lds = false;
     for (int32_t first = 0; first < n; first += KVIO_MAX_SPANS_PER_LAUNCH) {
         const int32_t cnt = n - first < KVIO_MAX_SPANS_PER_LAUNCH ? n - first : KVIO_MAX_SPANS_PER_LAUNCH;
         kvio::CopyArgs a;
-        memset(&a, 0, sizeof a);
-        a.layers = p->d_layers;
-        a.err = p->d_err;
-        a.row_bytes = R;
-        a.num_pages = p->num_slots / p->page_size;
-        a.num_layers = p->num_layers;
-        a.layer_begin = l0;
-        a.page_size = p->page_size;
-        a.page_shift = ilog2_exact(p->page_size);
-        a.vec_per_row = static_cast<int32_t>(R / 16);
-        a.vec_shift = ilog2_exact(R / 16);
-        a.rows_per_tile = rpt;
+        kvio::common_args(p, shape, l0, &a);
         a.n_spans = cnt;
-        a.host_layout = p->host_layout;
-        a.num_heads = p->num_heads;
-        a.seg_vecs = static_cast<int32_t>(p->seg_bytes / 16);
         int64_t tiles = 0;
         for (int32_t i = 0; i < cnt; ++i) {
             const Resolved &r = rs[size_t(first + i)];
@@ -454,17 +439,13 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
             a.spans[i].host_tokens = r.host_tokens;
             a.spans[i].num_tokens = static_cast<int32_t>(r.num_tokens);
             a.spans[i].origin = first + i;
-            tiles += (r.num_tokens + rpt - 1) / rpt;
+            tiles += (r.num_tokens + a.rows_per_tile - 1) / a.rows_per_tile;
         }
         a.tile_prefix[cnt] = tiles;
         a.plane_tiles = tiles;
         a.total_tiles = tiles * 2 * int64_t(l1 - l0);
         if (a.total_tiles == 0) continue;
-        kvio::Shape s = shape;
-        const int64_t waves_per_wg = s.threads / 64;
-        const int64_t max_wgs = (a.total_tiles + waves_per_wg - 1) / waves_per_wg;
-        if (s.workgroups > max_wgs) s.workgroups = static_cast<int>(max_wgs);
-        hipError_t e = kvio::launch_copy(a, dir, s, stream);
+        const hipError_t e = kvio::launch_capped(a, dir, shape, stream);
         if (e != hipSuccess) return fail_hip(e, fn);
     }
     return KVIO_OK;

@@ -127,53 +127,59 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
     int64_t layer_bytes = 0;                  // one layer of every span
     for (int32_t s = 0; s < n; ++s) layer_bytes += 2 * rs[size_t(s)].num_tokens * R;
     if (layer_bytes == 0) return KVIO_OK;
-    for (int32_t l = l0; l < l1;) {
-        if (layer_bytes <= cap) {
-            // whole spans over g layers per slot
-            const int32_t g = int32_t(std::min<int64_t>(l1 - l, cap / layer_bytes));
+    auto plan = [&]() -> kvio_status {
+        for (int32_t l = l0; l < l1;) {
+            if (layer_bytes <= cap) {
+                // whole spans over g layers per slot
+                const int32_t g = int32_t(std::min<int64_t>(l1 - l, cap / layer_bytes));
+                for (int32_t s = 0; s < n; ++s) {
+                    const int64_t T = rs[size_t(s)].num_tokens;
+                    if (T == 0) continue;
+                    if (units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
+                        kvio_status st = flush(l, g);
+                        if (st != KVIO_OK) return st;
+                    }
+                    units.push_back({s, 0, T, used});
+                    used += int64_t(g) * 2 * T * R;
+                }
+                kvio_status st = flush(l, g);
+                if (st != KVIO_OK) return st;
+                l += g;
+                continue;
+            }
+            // one layer per slot, spans split into runs of whole pages
             for (int32_t s = 0; s < n; ++s) {
                 const int64_t T = rs[size_t(s)].num_tokens;
-                if (T == 0) continue;
-                if (units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
-                    kvio_status st = flush(l, g);
-                    if (st != KVIO_OK) return st;
+                int64_t t0 = 0;
+                while (t0 < T) {
+                    const int64_t room = (cap - used) / (2 * R);
+                    const int64_t take = T - t0 <= room ? T - t0 : room / P * P;
+                    if (take == 0 || units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
+                        if (units.empty()) return fail(KVIO_EINVAL, "%s: staging slot below one page", fn);
+                        kvio_status st = flush(l, 1);
+                        if (st != KVIO_OK) return st;
+                        continue;
+                    }
+                    units.push_back({s, t0, take, used});
+                    used += 2 * take * R;
+                    t0 += take;
                 }
-                units.push_back({s, 0, T, used});
-                used += int64_t(g) * 2 * T * R;
             }
-            kvio_status st = flush(l, g);
+            kvio_status st = flush(l, 1);
             if (st != KVIO_OK) return st;
-            l += g;
-            continue;
+            ++l;
         }
-        // one layer per slot, spans split into runs of whole pages
-        for (int32_t s = 0; s < n; ++s) {
-            const int64_t T = rs[size_t(s)].num_tokens;
-            int64_t t0 = 0;
-            while (t0 < T) {
-                const int64_t room = (cap - used) / (2 * R);
-                const int64_t take = T - t0 <= room ? T - t0 : room / P * P;
-                if (take == 0 || units.size() == size_t(KVIO_MAX_SPANS_PER_LAUNCH)) {
-                    if (units.empty()) return fail(KVIO_EINVAL, "%s: staging slot below one page", fn);
-                    kvio_status st = flush(l, 1);
-                    if (st != KVIO_OK) return st;
-                    continue;
-                }
-                units.push_back({s, t0, take, used});
-                used += 2 * take * R;
-                t0 += take;
-            }
-        }
-        kvio_status st = flush(l, 1);
-        if (st != KVIO_OK) return st;
-        ++l;
-    }
+        return KVIO_OK;
+    };
+    const kvio_status st = plan();
+    // A load joins the side stream back even when a later slot failed, so the
+    // next call's copies cannot refill a slot that a queued scatter still reads.
     if (dir == kvio::kLoad && chunk > 0) {
         e = hipEventRecord(p->ev_done[dir], ks);
         if (e == hipSuccess) e = hipStreamWaitEvent(stream, p->ev_done[dir], 0);
-        if (e != hipSuccess) return fail_hip(e, fn);
+        if (e != hipSuccess && st == KVIO_OK) return fail_hip(e, fn);
     }
-    return KVIO_OK;
+    return st;
 }
 
 }  // namespace kvio
