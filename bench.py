@@ -13,7 +13,8 @@ Reported (one JSON line):
               payload bytes / mean step time; inputs are resident (host chunk
               pinned, pool in HBM) before the timed region.
   load/offload per-direction GB/s and tokens/s, each against the measured
-              contiguous hipMemcpyAsync peak of the same direction on this machine.
+              contiguous hipMemcpyAsync peak of the same direction, measured in the
+              same run.
   roofline    the load kernel (the critical-path direction): algorithmic
               bytes per launch / mean launch time from HIP events on its
               stream, against the published PCIe Gen5 x16 rate (64 GB/s),
@@ -27,7 +28,7 @@ Other workloads: --config 1 (tiny pool, P = 16), --config 3 (70B KV, P = 16,
 layer-wise load on a side stream against a per-layer bf16 GEMM), --config 4
 (64 batched partial hits in a churned pool), --config 5 (1M-token load with
 concurrent offloads); --staged (copy engine + HBM scatter), --interference,
---page-sweep, --schedule, --disk.
+--page-sweep, --row-sweep, --schedule, --disk.
 """
 from __future__ import annotations
 
@@ -512,8 +513,8 @@ def run_layerwise(args, torch, kv, W):
 def run_batched(args, torch, kv, W):
     """64 partial-hit contexts of the 8B shape at page size 16 into a pool
     fragmented by a seeded allocate/free churn; one batched kvio_load per wave
-    of contexts (pinned host memory per process is capped on the box, so the
-    host chunks are staged in waves of <= 40 GiB)."""
+    of contexts (pinned host memory per process may be capped, at 64 GiB on
+    some machines, so the host chunks are staged in waves of <= 40 GiB)."""
     k = 4
     shp = W.LLAMA8B
     L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
@@ -1265,7 +1266,7 @@ EXTRA_MODES = {3: run_layerwise, 4: run_batched, 5: run_bidirectional}
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the transfer path has no "
+        print(json.dumps({"error": "kvio moves one GPU's KV over its own host link and has no "
                                    "cross-GPU step; run with --gpus 1"}))
         sys.exit(2)
     import torch

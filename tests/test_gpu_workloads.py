@@ -139,7 +139,7 @@ def test_workload4_batched_churned(kv):
     S = req.pool_pages * P
     hit = [int(h) for h in req.hit_tokens]
     sizes = [L * 2 * h * R for h in hit]
-    # Pinned host memory on the test box is capped (64 GiB per process), so the
+    # Pinned host memory per process may be capped (64 GiB on some machines), so the
     # contexts are loaded in waves of at most 40 GiB of host chunks, each wave
     # one batched kvio_load; the pool holds all of them.
     budget = 40 * GiB
@@ -228,8 +228,8 @@ def test_workload5_1m_with_concurrent_offload(kv, io_stream, staged):
         spans_np = [(hb.array, T, T, load_slots), (src_o.array, TO, TO, off_slots)]
         sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k)
         untouched_rows_hold_sentinel(pool_t, touched_mask(spans_np, P, S), L)
-        # Round trip in token ranges through a 4 GiB chunk (pinned memory is
-        # capped at 64 GiB per process on the test box): offloading tokens
+        # Round trip in token ranges through a 4 GiB chunk (pinned memory per
+        # process may be capped at 64 GiB): offloading tokens
         # [a, b) uses the page table from entry a and a chunk of b - a tokens.
         piece = (4 * GiB) // (L * 2 * R)
         with kv.HostBuffer(L * 2 * piece * R) as ob:
