@@ -82,6 +82,8 @@ SHAPES = [
     (2, 6, 128, 4, 600, [(201, 204)]),                  # R = 1536 B (odd vectors)
     (2, 2, 64, 5, 1000, [(123, 125), (0, 5)]),          # R = 256 B, P = 5, empty span
     (2, 128, 128, 1, 64, [(10, 12)]),                   # R = 32 KiB: wider than a step
+    (1, 4, 64, 100, 1000, [(250, 300), (100, 100)]),    # P = 100 (no shift), page > one tile
+    (1, 1, 8, 128, 128, [(100, 128)]),                  # a one-page pool, R = 16 B
 ]
 
 

@@ -105,6 +105,10 @@ def run_case(kv, L, H, D, P, S, spans, l0=0, l1=None, launch=None, seed=0, shape
     (2, 8, 128, 32, 4096, [(500, 512), (64, 64)]),        # P = 32
     (2, 8, 128, 64, 4096, [(1000, 1000)]),                # P = 64
     (2, 2, 64, 5, 1000, [(123, 130), (44, 50)]),          # R = 256 B, P = 5
+    (2, 8, 128, 1, 1, [(1, 1)]),                          # a one-slot pool
+    (1, 1, 8, 128, 128, [(100, 128)]),                    # a one-page pool, page > one tile
+    (2, 8, 128, 256, 1024, [(700, 768)]),                 # P = 256: pages span several tiles
+    (1, 4, 64, 100, 1000, [(250, 300), (100, 100)]),      # P = 100 (no shift), > one tile
 ])
 def test_parity_shapes(kv, L, H, D, P, S, spans):
     run_case(kv, L, H, D, P, S, spans, seed=L * 31 + P)
