@@ -48,6 +48,7 @@ sys.path.insert(0, ROOT)
 GB = 1e9
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor figure
 PCIE_SPEC_GBPS = 64.0           # PCIe Gen5 x16 per direction (raw)
+BIDIR_OVERLAP = 1.3             # H2D || D2H counts as overlapped above this x the faster direction
 
 
 def parse():
@@ -217,9 +218,43 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
             torch.cuda.synchronize()
             ts.append(time.perf_counter() - t0)
         best = max(best, 2 * half / statistics.median(ts) / GB)
-    res["bidir"] = best
+    # In a few processes every pair above serialises; fresh HIP streams (new
+    # runtime queues) are tried next, and if the two directions still never
+    # overlap the bidirectional peak is reported as unmeasured, not as the
+    # one-direction rate.
+    overlap = BIDIR_OVERLAP * max(res["h2d"], res["d2h"])
+    fresh = []
+    try:
+        while best < overlap and len(fresh) < 6:
+            fresh.append(kv.Stream())
+            for a, b in ((s1, fresh[-1].torch), (null, fresh[-1].torch)):
+                ts = []
+                for _ in range(reps):
+                    torch.cuda.synchronize()
+                    t0 = time.perf_counter()
+                    kv.kvio_memcpy(dev_ptr, src_ptr, half, a)
+                    kv.kvio_memcpy(dst_ptr + half, dev_ptr + half, half, b)
+                    torch.cuda.synchronize()
+                    ts.append(time.perf_counter() - t0)
+                best = max(best, 2 * half / statistics.median(ts) / GB)
+    finally:
+        for f in fresh:
+            f.close()
+    if best >= overlap:
+        res["bidir"] = best
+    else:
+        res["bidir"] = None
+        res["bidir_note"] = (f"unmeasured: the runtime serialised H2D and D2H copies on every stream pair "
+                             f"tried in this process (best {best:.2f} GB/s)")
     res["bytes"] = nbytes
     return res
+
+
+def peak_report(peak):
+    """The measured memcpy peaks for the JSON line (GB/s rounded)."""
+    if not peak:
+        return None
+    return {k: round(v, 3) if isinstance(v, float) else v for k, v in peak.items()}
 
 
 def cpu_model():
@@ -360,7 +395,8 @@ def h2d_d2h_peak(torch, kv, nbytes=2 << 30):
         hb.array[::4096] = 1                      # touch every page once
         peak = memcpy_peak(torch, kv, hb.ptr, hb.ptr, scratch.data_ptr(), nbytes)
     del scratch
-    log(f"memcpy peak: h2d {peak['h2d']:.2f} GB/s, d2h {peak['d2h']:.2f} GB/s, bidir {peak['bidir']:.2f} GB/s")
+    bidir = f"{peak['bidir']:.2f} GB/s" if peak["bidir"] else peak["bidir_note"]
+    log(f"memcpy peak: h2d {peak['h2d']:.2f} GB/s, d2h {peak['d2h']:.2f} GB/s, bidir {bidir}")
     _PEAK["peak"] = peak
     return peak
 
@@ -501,7 +537,7 @@ def run_layerwise(args, torch, kv, W):
                       "load_gbps_corun": round(load_gbps_co, 3), "gemm_slowdown": round(tg_co / tg, 4),
                       "gemm_tflops_alone": round(gemm_tflops, 1)},
         "load": {"gbps": round(load_gbps_co, 3), "frac_of_h2d_peak": round(load_gbps_co / peak["h2d"], 4) if peak else None},
-        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "host_link_peak": peak_report(peak),
         "roofline": roofline("kvio_copy_kernel<load> (per layer)", load_gbps, peak["h2d"] if peak else None,
                              algorithmic_bytes_per_launch=per_layer),
     })
@@ -582,7 +618,7 @@ def run_batched(args, torch, kv, W):
         "offload": {"gbps": round(off_gbps, 3), "ms": round(toff, 3),
                     "frac_of_d2h_peak": round(off_gbps / peak["d2h"], 4) if peak else None},
         "wave_load_ms": [round(x, 3) for x in load_ms],
-        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "host_link_peak": peak_report(peak),
         "roofline": roofline("kvio_copy_kernel<load> (batched spans)", load_gbps, peak["h2d"] if peak else None,
                              algorithmic_bytes_per_launch=round(total / len(waves))),
     })
@@ -686,8 +722,8 @@ def run_bidirectional(args, torch, kv, W):
                     "gbps_alone": round(nbo / (t_off_alone * 1e-3) / GB, 3),
                     "frac_of_d2h_peak_alone": round(nbo / (t_off_alone * 1e-3) / GB / peak["d2h"], 4) if peak else None},
         "bidirectional_gbps": round(bidir, 3),
-        "frac_of_bidir_peak": round(bidir / peak["bidir"], 4) if peak else None,
-        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "frac_of_bidir_peak": round(bidir / peak["bidir"], 4) if peak and peak["bidir"] else None,
+        "host_link_peak": peak_report(peak),
         "roofline": roofline("kvio_copy_kernel<load> || <offload>", bidir, peak["bidir"] if peak else None,
                              directions=2, algorithmic_bytes_per_launch=nb),
     })
@@ -871,7 +907,7 @@ def run_row_sweep(args, torch, kv, W):
                       "row-size sweep: 80 layers, 1..32 KV heads x 128 dims bf16, 2 GiB per direction, "
                       "page sizes 1 and 16", {})
     res["metric"] = "kvio load / offload GB/s against the token row size"
-    res["host_link_peak"] = {k2: round(v, 3) for k2, v in peak.items()} if peak else None
+    res["host_link_peak"] = peak_report(peak)
     res["sweep"] = rows
     print(json.dumps(res), flush=True)
 
@@ -958,7 +994,7 @@ def run_page_sweep(args, torch, kv, W):
                       "page-size sweep: Llama-3.1-8B KV, 32K tokens at page sizes 1..256 and 8192 tokens at "
                       "page size 32, pool of 2^19 slots", {"pool_slots": S})
     res["metric"] = "kvio vs per-page hipMemcpyAsync load GB/s against page size"
-    res["host_link_peak"] = {k2: round(v, 3) for k2, v in peak.items()} if peak else None
+    res["host_link_peak"] = peak_report(peak)
     res["sweep"] = rows
     print(json.dumps(res), flush=True)
 
@@ -1459,7 +1495,7 @@ def run_single(args, torch, kv, W, k):
                     "tokens_per_s": round(T / (off_ms * 1e-3), 1),
                     "frac_of_d2h_peak": round(frac_d2h, 4) if peak else None},
         "frac_of_host_link_peak": round(ideal_ms / step_ms, 4) if peak else None,
-        "host_link_peak": {k2: round(v, 3) for k2, v in peak.items()} if peak else None,
+        "host_link_peak": peak_report(peak),
         "roofline": roofline("kvio_copy_kernel<load>" + (" (staged)" if args.staged else ""), load_gbps,
                              peak["h2d"] if peak else None, traffic=traffic,
                              algorithmic_bytes_per_launch=payload, algorithmic_traffic_per_launch=2 * payload),

@@ -92,3 +92,14 @@ def test_memequal_np_stops_at_n():
     b[(2 << 20) + 5:] = 1
     assert bench.memequal_np(a, b, (2 << 20) + 5)
     assert not bench.memequal_np(a, b, (2 << 20) + 6)
+
+
+def test_peak_report_keeps_an_unmeasured_bidirectional_peak():
+    assert bench.peak_report(None) is None
+    ok = bench.peak_report({"h2d": 57.30512, "d2h": 57.0391, "bidir": 97.3049, "bytes": 2 << 30})
+    assert ok == {"h2d": 57.305, "d2h": 57.039, "bidir": 97.305, "bytes": 2 << 30}
+    note = "unmeasured: the runtime serialised H2D and D2H copies"
+    r = bench.peak_report({"h2d": 57.3, "d2h": 57.0, "bidir": None, "bidir_note": note, "bytes": 2 << 30})
+    assert r["bidir"] is None and r["bidir_note"] == note
+    # the roofline of the bidirectional workload then has no measured ceiling
+    assert bench.roofline("k", 88.0, r["bidir"], directions=2)["frac_of_measured_peak"] is None
