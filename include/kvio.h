@@ -45,8 +45,9 @@
  *   - A pool handle is immutable after creation and may be used from several
  *     threads and streams at once.  Transfers that run concurrently must write
  *     disjoint bytes (and staged transfers of one direction must not overlap);
- *     a load whose page tables name one pool slot twice leaves that slot
- *     holding one of the rows (unspecified which).
+ *     a load whose page tables name one pool slot twice leaves each 16-byte
+ *     piece of that slot holding the same piece of one of the rows named
+ *     for it (unspecified which; the pieces may come from different rows).
  *   - Page indices are range-checked on the device at no measurable cost: a
  *     row whose page lies outside [0, S / P) is skipped, never dereferenced,
  *     and the first such (span, context page) is recorded for kvio_check().

@@ -437,3 +437,83 @@ def test_undersized_buffers_rejected(kv):
     finally:
         torch.cuda.synchronize()
         hip.hipFree(dev)
+
+
+@pytest.mark.parametrize("staged", [False, True])
+def test_offload_reads_shared_and_repeated_pages(kv, staged):
+    """Offload may name a pool page any number of times: contexts that share a
+    prefix page, a page repeated inside one table.  Every host row receives its
+    page's row, as the oracle's offload gives."""
+    import torch
+    L, H, D, P, S = 2, 4, 64, 16, 1024
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 55)
+    pages = np.random.default_rng(55).permutation(S // P)[:6].astype(np.int32)
+    tables = [pages[:6],                                        # context A
+              np.concatenate([pages[:4], pages[[0, 0, 5]]]),    # B shares A's first pages, repeats one
+              pages[[3, 3, 3]]]                                 # one page three times
+    lens = [6 * P - 5, 7 * P, 2 * P + 1]
+    launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None
+    pool = kv.KVPool(pool_t, P, offload_launch=launch, staging_bytes=4 * 2 * 2 * P * R if staged else 0)
+    outs, pts, ora = [], [], []
+    try:
+        for tab, T in zip(tables, lens):
+            ob = kv.HostBuffer(L * 2 * T * R)
+            ob.array[:] = 0x3C
+            outs.append(ob)
+            pts.append(torch.from_numpy(tab.copy()).cuda())
+            ora.append((np.full(ob.array.size, 0x3C, np.uint8), T, T, tab))
+        pool.offload([(ob.ptr, T, T, pt.data_ptr()) for ob, pt, (_, T, _, _) in zip(outs, pts, ora)])
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.offload(exp[0], exp[1], P, ora)
+        for i, ((eo, _, _, _), ob) in enumerate(zip(ora, outs)):
+            assert np.array_equal(ob.array, eo), f"offload span {i} differs from the oracle"
+        assert np.array_equal(_pool_bytes(pool_t), pool_np), "an offload changed the pool"
+    finally:
+        pool.close()
+        for ob in outs:
+            ob.free()
+
+
+def test_load_naming_a_slot_twice_fills_it_from_its_rows(kv):
+    """A load whose table names a page twice is the caller's mistake (the
+    oracle rejects it); the library promises only that each 16-byte piece of
+    such a slot holds that piece of one of the rows named for it.  Every other
+    slot gets exactly what the oracle gives for the same load without the
+    repeat."""
+    import torch
+    L, H, D, P, S = 2, 8, 128, 4, 256               # R = 2 KiB: rows span several 16-byte pieces
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 66)
+    pages = np.random.default_rng(66).permutation(S // P)[:3].astype(np.int32)
+    table = np.array([pages[0], pages[1], pages[0], pages[2]], np.int32)   # context pages 0 and 2 collide
+    T = 4 * P - 1
+    pool = kv.KVPool(pool_t, P)
+    with kv.HostBuffer(L * 2 * T * R) as hb:
+        W.fill_np(hb.array, 66, W.LLAMA8B)
+        pt = torch.from_numpy(table).cuda()
+        pool.load([(hb.ptr, T, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        pool.check()
+        got = _pool_bytes(pool_t)
+        # the oracle's load of context pages 1 and 3 only (no repeat)
+        exp = pool_np.copy()
+        host = hb.array.reshape(L, 2, T, R)
+        for j in (1, 3):
+            n = min(P, T - j * P)
+            sub = np.ascontiguousarray(host[:, :, j * P:j * P + n]).reshape(-1)
+            oracle.load(exp[0], exp[1], P, [(sub, n, n, table[j:j + 1])])
+        dup = set(range(int(pages[0]) * P, int(pages[0]) * P + P))
+        other = np.array([s not in dup for s in range(S)])
+        assert np.array_equal(got[:, :, other], exp[:, :, other]), "a slot outside the repeated page differs"
+        for o in range(P):
+            slot = int(pages[0]) * P + o
+            cands = [host[:, :, j * P + o] for j in (0, 2) if j * P + o < T]
+            pieces_got = got[:, :, slot].transpose(1, 0, 2).reshape(L, 2, R // 16, 16)   # (layer, kv, ...)
+            ok = np.zeros((L, 2, R // 16), bool)
+            for c in cands:
+                ok |= (pieces_got == c.reshape(L, 2, R // 16, 16)).all(axis=-1)
+            assert ok.all(), f"slot {slot}: a 16-byte piece matches none of its rows"
+    pool.close()
