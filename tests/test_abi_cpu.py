@@ -73,3 +73,17 @@ def test_host_side_validation_without_device():
     assert e.value.status == kv.KVIO_EINVAL
     kv.kvio_pool_destroy(0)                                     # NULL is accepted
     kv.kvio_memcpy(0, 0, 0)                                     # zero bytes: no-op
+
+
+def test_package_refuses_to_import_without_the_library(tmp_path):
+    """No fallback: without libkvio.so the package raises at import."""
+    import shutil
+    import subprocess
+    import sys
+    pkg = os.path.join(ROOT, "paper_2508_18572_amd")
+    shutil.copytree(pkg, tmp_path / "paper_2508_18572_amd",
+                    ignore=lambda d, names: [n for n in names if n.endswith(".so") or n == "__pycache__"])
+    r = subprocess.run([sys.executable, "-c", "import paper_2508_18572_amd"], cwd=tmp_path,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "is not built" in r.stderr
