@@ -517,3 +517,62 @@ def test_load_naming_a_slot_twice_fills_it_from_its_rows(kv):
                 ok |= (pieces_got == c.reshape(L, 2, R // 16, 16)).all(axis=-1)
             assert ok.all(), f"slot {slot}: a 16-byte piece matches none of its rows"
     pool.close()
+
+
+def test_one_pool_from_several_host_threads(kv):
+    """One pool handle used by four host threads at once, each on its own
+    stream with its own context in pages no other thread touches (ctypes
+    releases the interpreter lock during the calls).  Each thread also makes an
+    invalid call and must read its own error text (the text is per thread)."""
+    import threading
+    import torch
+    L, H, D, P, S = 2, 8, 128, 16, 8192
+    R = H * D * 2
+    n_threads, T = 4, 300
+    need = -(-T // P)
+    pool_np, pool_t = _pool(L, S, H, D, 88)
+    perm = np.random.default_rng(88).permutation(S // P)[:n_threads * need].astype(np.int32)
+    tables = [perm[i * need:(i + 1) * need] for i in range(n_threads)]
+    pts = [torch.from_numpy(t.copy()).cuda() for t in tables]
+    streams = [torch.cuda.Stream() for _ in range(n_threads)]
+    hbs = [kv.HostBuffer(L * 2 * T * R) for _ in range(n_threads)]
+    obs = [kv.HostBuffer(L * 2 * T * R) for _ in range(n_threads)]
+    pool = kv.KVPool(pool_t, P)
+    failures = [None] * n_threads
+    try:
+        for i in range(n_threads):
+            W.fill_np(hbs[i].array, 880 + i, W.LLAMA8B)
+            obs[i].array[:] = 0
+        torch.cuda.synchronize()
+
+        def work(i):
+            try:
+                span_in = [(hbs[i].ptr, T, T, pts[i].data_ptr())]
+                span_out = [(obs[i].ptr, T, T, pts[i].data_ptr())]
+                for _ in range(10):
+                    pool.load(span_in, stream=streams[i])
+                    pool.offload(span_out, stream=streams[i])
+                    with pytest.raises(kv.KvioError) as e:
+                        pool.load(span_in, 0, L + 1 + i, stream=streams[i])
+                    assert f"[0, {L + 1 + i})" in e.value.detail, e.value.detail
+                streams[i].synchronize()
+            except BaseException as exc:          # reported by the main thread
+                failures[i] = exc
+
+        threads = [threading.Thread(target=work, args=(i,)) for i in range(n_threads)]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        assert failures == [None] * n_threads, failures
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, [(hbs[i].array, T, T, tables[i]) for i in range(n_threads)])
+        assert np.array_equal(_pool_bytes(pool_t), exp), "pool differs from the oracle"
+        for i in range(n_threads):
+            assert np.array_equal(obs[i].array, hbs[i].array), f"thread {i}: round trip differs"
+    finally:
+        pool.close()
+        for b in hbs + obs:
+            b.free()
