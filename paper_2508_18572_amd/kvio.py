@@ -23,6 +23,7 @@ import torch  # noqa: F401  (binds the HIP runtime before libkvio.so loads)
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libkvio.so")
 
+# kvio_status
 KVIO_OK = 0
 KVIO_EINVAL = -1
 KVIO_ERANGE = -2
@@ -30,16 +31,20 @@ KVIO_EALIGN = -3
 KVIO_ENOTMAPPED = -4
 KVIO_EHIP = -5
 KVIO_ENOMEM = -6
+KVIO_EIO = -7
 
+# host chunk layouts
 KVIO_HOST_TOKEN_MAJOR = 0
 KVIO_HOST_PAGE_FIRST = 1
 KVIO_HOST_HEAD_MAJOR = 2
+# launch flags
 KVIO_LAUNCH_CACHED = 0x1
 KVIO_LAUNCH_NO_LDS = 0x2
 KVIO_LAUNCH_STAGED = 0x4
-KVIO_EIO = -7
+# disk store layouts
 KVIO_DISK_PAGE_FIRST = 0
 KVIO_DISK_LAYER_FIRST = 1
+# pinned host memory flags
 KVIO_HOST_COHERENT = 0x0
 KVIO_HOST_NONCOHERENT = 0x1
 KVIO_MAX_SPANS_PER_LAUNCH = 64

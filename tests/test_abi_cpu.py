@@ -87,3 +87,52 @@ def test_package_refuses_to_import_without_the_library(tmp_path):
                        capture_output=True, text=True, timeout=300)
     assert r.returncode != 0
     assert "ImportError" in r.stderr and "is not built" in r.stderr
+
+
+def test_python_constants_match_the_header():
+    import paper_2508_18572_amd.kvio as K
+    text = open(os.path.join(ROOT, "include", "kvio.h")).read()
+    consts = {m.group(1): int(m.group(2), 0)
+              for m in re.finditer(r"#define (KVIO_[A-Z0-9_]+) (0x[0-9a-fA-F]+|-?\d+)\b", text)}
+    consts.update({m.group(1): int(m.group(2))
+                   for m in re.finditer(r"\b(KVIO_E[A-Z]+|KVIO_OK) = (-?\d+)", text)})
+    assert len(consts) >= 19          # 8 status codes and 11 #defines
+    for name, value in consts.items():
+        assert getattr(K, name) == value, name
+
+
+STRUCTS = {
+    "kvio_launch": ["workgroups", "threads", "tile_kib", "flags"],
+    "kvio_pool_desc": ["num_layers", "num_kv_heads", "head_dim", "elem_bytes", "page_size", "host_layout",
+                       "num_slots", "k_layers", "v_layers", "load_launch", "offload_launch", "staging_bytes"],
+    "kvio_span": ["host", "host_tokens", "num_tokens", "page_idx"],
+    "kvio_request": ["load_tokens", "compute_tokens", "context", "transient_matches"],
+    "kvio_batch_policy": ["max_tokens", "max_requests", "reserved", "loading_bound_ratio", "delay_hit_threshold"],
+    "kvio_disk_store": ["fd", "disk_layout", "num_disk_pages", "num_layers", "page_size", "row_bytes"],
+}
+
+
+def test_ctypes_structs_match_the_c_layout(tmp_path):
+    """Every struct the binding passes across the ABI has the size and field
+    offsets gcc gives the header's declaration."""
+    import subprocess
+    import paper_2508_18572_amd.kvio as K
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "kvio.h"', "int main(void) {"]
+    for st, fields in STRUCTS.items():
+        lines.append(f'    printf("{st} size %zu\\n", sizeof({st}));')
+        for f in fields:
+            lines.append(f'    printf("{st} {f} %zu\\n", offsetof({st}, {f}));')
+    lines += ["    return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = str(tmp_path / "layout")
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), str(src), "-o", exe],
+                   check=True)
+    out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split("\n")
+    c = {(a, b): int(v) for a, b, v in (ln.split() for ln in out if ln)}
+    for st, fields in STRUCTS.items():
+        cls = getattr(K, st)
+        assert [f[0] for f in cls._fields_] == fields, st
+        assert ctypes.sizeof(cls) == c[(st, "size")], st
+        for f in fields:
+            assert getattr(cls, f).offset == c[(st, f)], (st, f)
