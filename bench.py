@@ -1496,7 +1496,8 @@ def run_single(args, torch, kv, W, k):
                     "frac_of_d2h_peak": round(frac_d2h, 4) if peak else None},
         "frac_of_host_link_peak": round(ideal_ms / step_ms, 4) if peak else None,
         "host_link_peak": peak_report(peak),
-        "roofline": roofline("kvio_copy_kernel<load>" + (" (staged)" if args.staged else ""), load_gbps,
+        "roofline": roofline(("kvio_head_major_kernel<load>" if args.host_layout == "head" else "kvio_copy_kernel<load>")
+                             + (" (staged)" if args.staged else ""), load_gbps,
                              peak["h2d"] if peak else None, traffic=traffic,
                              algorithmic_bytes_per_launch=payload, algorithmic_traffic_per_launch=2 * payload),
         "naive": naive,
