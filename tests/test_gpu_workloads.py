@@ -127,9 +127,11 @@ def test_workload3_staged_layerwise(kv, io_stream):
     single_context_workload(kv, 3, io_stream, layerwise=True, staged=True)
 
 
-def test_workload4_batched_churned(kv):
+@pytest.mark.parametrize("staged", [False, True], ids=["kernel", "staged"])
+def test_workload4_batched_churned(kv, staged):
     """64 partial-hit contexts of the 8B shape at page size 16 into a churned pool,
-    one batched kvio_load per wave (one wave when host memory allows)."""
+    one batched kvio_load per wave (one wave when host memory allows); staged:
+    both directions through the default 4 GiB of HBM staging each."""
     import torch
     k = 4
     shp = W.LLAMA8B
@@ -152,9 +154,11 @@ def test_workload4_batched_churned(kv):
         acc += b
     waves.append(cur)
     print(f"[workload4] {sum(hit)} tokens, {sum(sizes) / GiB:.1f} GiB, pool {S} slots, "
-          f"{len(waves)} wave(s), mean run length {req.mean_run_length:.2f}", flush=True)
+          f"{len(waves)} wave(s), mean run length {req.mean_run_length:.2f}, staged {staged}", flush=True)
+    torch.cuda.empty_cache()                 # the pool takes most of HBM
     pool_t = new_pool(L, S, H, D, torch.bfloat16)
-    pool = kv.KVPool(pool_t, P)
+    launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None
+    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
     pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
     all_spans_np = []
     for w in waves:
