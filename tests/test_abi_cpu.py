@@ -73,6 +73,14 @@ def test_host_side_validation_without_device():
     assert e.value.status == kv.KVIO_EINVAL
     kv.kvio_pool_destroy(0)                                     # NULL is accepted
     kv.kvio_memcpy(0, 0, 0)                                     # zero bytes: no-op
+    lib = kv.kvio._lib                                          # stream arguments, checked before HIP
+    out = ctypes.c_void_p()
+    zero = (ctypes.c_uint32 * 2)()
+    assert lib.kvio_stream_create(zero, 2, ctypes.byref(out)) == kv.KVIO_EINVAL
+    assert "empty CU mask" in kv.kvio_last_error()
+    assert lib.kvio_stream_create(None, 1, ctypes.byref(out)) == kv.KVIO_EINVAL
+    assert lib.kvio_stream_create(None, 0, None) == kv.KVIO_EINVAL
+    assert lib.kvio_stream_destroy(None) == kv.KVIO_EINVAL
 
 
 def test_package_refuses_to_import_without_the_library(tmp_path):

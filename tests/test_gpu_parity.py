@@ -576,3 +576,38 @@ def test_one_pool_from_several_host_threads(kv):
         pool.close()
         for b in hbs + obs:
             b.free()
+
+
+def test_transfers_on_a_stream_masked_to_16_cus(kv):
+    """kvio_stream_create with a CU mask of 16 compute units (the load's default
+    quota): a load and an offload on that stream match the oracle.  The runtime
+    allows few masked streams per process; if it refuses one more, the test is
+    skipped."""
+    import torch
+    try:
+        st = kv.Stream(list(range(16)))
+    except kv.KvioError as e:
+        pytest.skip(f"the runtime refused another CU-masked stream: {e.detail}")
+    try:
+        L, H, D, P, S = 2, 8, 128, 16, 4096
+        R = H * D * 2
+        pool_np, pool_t = _pool(L, S, H, D, 99)
+        T = 1500
+        pages = np.random.default_rng(99).permutation(S // P)[:-(-T // P)].astype(np.int32)
+        pt = torch.from_numpy(pages).cuda()
+        pool = kv.KVPool(pool_t, P)
+        with kv.HostBuffer(L * 2 * T * R) as hb, kv.HostBuffer(L * 2 * T * R) as ob:
+            W.fill_np(hb.array, 99, W.LLAMA8B)
+            ob.array[:] = 0
+            torch.cuda.synchronize()
+            pool.load([(hb.ptr, T, T, pt.data_ptr())], stream=st)
+            pool.offload([(ob.ptr, T, T, pt.data_ptr())], stream=st)
+            torch.cuda.synchronize()
+            pool.check()
+            exp = pool_np.copy()
+            oracle.load(exp[0], exp[1], P, [(hb.array, T, T, pages)])
+            assert np.array_equal(_pool_bytes(pool_t), exp)
+            assert np.array_equal(ob.array, hb.array)
+        pool.close()
+    finally:
+        st.close()
