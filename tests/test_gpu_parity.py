@@ -611,3 +611,37 @@ def test_transfers_on_a_stream_masked_to_16_cus(kv):
         pool.close()
     finally:
         st.close()
+
+
+@pytest.mark.parametrize("layout,staged", [(0, False), (0, True), (2, False), (2, True)])
+def test_noncoherent_host_chunks(kv, layout, staged):
+    """Coarse-grained (non-coherent) pinned host chunks: the offload's host
+    writes are visible to the CPU after synchronisation and both directions
+    match the oracle, on the kernel path and staged."""
+    import torch
+    L, H, D, P, S = 2, 8, 128, 16, 4096
+    R = H * D * 2
+    T, HT = 1000, 1010
+    pool_np, pool_t = _pool(L, S, H, D, 101 + layout)
+    pages = np.random.default_rng(101).permutation(S // P)[:-(-T // P)].astype(np.int32)
+    pt = torch.from_numpy(pages).cuda()
+    launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None
+    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch, host_layout=layout,
+                     staging_bytes=4 * 4 * 2 * P * R if staged else 0)
+    ora_layout = {0: oracle.TOKEN_MAJOR, 2: oracle.HEAD_MAJOR}[layout]
+    nbytes = oracle.host_chunk_bytes(ora_layout, L, HT, R, P)
+    with kv.HostBuffer(nbytes, kv.KVIO_HOST_NONCOHERENT) as hb, \
+            kv.HostBuffer(nbytes, kv.KVIO_HOST_NONCOHERENT) as ob:
+        W.fill_np(hb.array, 101, W.LLAMA8B)
+        ob.array[:] = 0x77
+        pool.load([(hb.ptr, HT, T, pt.data_ptr())])
+        pool.offload([(ob.ptr, HT, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load_layout(exp[0], exp[1], P, [(hb.array, HT, T, pages)], ora_layout, num_heads=H)
+        assert np.array_equal(_pool_bytes(pool_t), exp), "load differs from the oracle"
+        exp_out = np.full(nbytes, 0x77, np.uint8)
+        oracle.offload_layout(exp[0], exp[1], P, [(exp_out, HT, T, pages)], ora_layout, num_heads=H)
+        assert np.array_equal(ob.array, exp_out), "offload differs from the oracle"
+    pool.close()
