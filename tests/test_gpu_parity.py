@@ -645,3 +645,34 @@ def test_noncoherent_host_chunks(kv, layout, staged):
         oracle.offload_layout(exp[0], exp[1], P, [(exp_out, HT, T, pages)], ora_layout, num_heads=H)
         assert np.array_equal(ob.array, exp_out), "offload differs from the oracle"
     pool.close()
+
+
+@pytest.mark.parametrize("layout", [0, 1, 2])
+def test_chunks_in_device_memory(kv, layout):
+    """A span's chunk may be device memory (a contiguous copy of the context
+    kept in HBM): the same layout conversion, HBM to HBM, matches the oracle."""
+    import torch
+    L, H, D, P, S = 2, 8, 128, 16, 4096
+    R = H * D * 2
+    T, HT = 777, 784                               # HT: whole pages, valid for every layout
+    pool_np, pool_t = _pool(L, S, H, D, 111 + layout)
+    pages = np.random.default_rng(111).permutation(S // P)[:-(-T // P)].astype(np.int32)
+    pt = torch.from_numpy(pages).cuda()
+    ora_layout = {0: oracle.TOKEN_MAJOR, 1: oracle.PAGE_FIRST, 2: oracle.HEAD_MAJOR}[layout]
+    nbytes = oracle.host_chunk_bytes(ora_layout, L, HT, R, P)
+    src = np.zeros(nbytes, np.uint8)
+    W.fill_np(src, 111, W.LLAMA8B)
+    d_src = torch.from_numpy(src).cuda()
+    d_out = torch.full((nbytes,), 0x55, dtype=torch.uint8, device="cuda")
+    pool = kv.KVPool(pool_t, P, host_layout=layout)
+    pool.load([(d_src.data_ptr(), HT, T, pt.data_ptr())])
+    pool.offload([(d_out.data_ptr(), HT, T, pt.data_ptr())])
+    torch.cuda.synchronize()
+    pool.check()
+    exp = pool_np.copy()
+    oracle.load_layout(exp[0], exp[1], P, [(src, HT, T, pages)], ora_layout, num_heads=H)
+    assert np.array_equal(_pool_bytes(pool_t), exp), "load differs from the oracle"
+    exp_out = np.full(nbytes, 0x55, np.uint8)
+    oracle.offload_layout(exp[0], exp[1], P, [(exp_out, HT, T, pages)], ora_layout, num_heads=H)
+    assert np.array_equal(d_out.cpu().numpy(), exp_out), "offload differs from the oracle"
+    pool.close()
