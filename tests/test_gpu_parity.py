@@ -676,3 +676,38 @@ def test_chunks_in_device_memory(kv, layout):
     oracle.offload_layout(exp[0], exp[1], P, [(exp_out, HT, T, pages)], ora_layout, num_heads=H)
     assert np.array_equal(d_out.cpu().numpy(), exp_out), "offload differs from the oracle"
     pool.close()
+
+
+def test_staged_load_and_offload_concurrently_on_one_handle(kv):
+    """Both directions staged on one pool handle, a load of context X on one
+    stream while an offload of context Y (other pages) runs on another, several
+    times over without host synchronisation: each direction has its own staging
+    slots and side stream, so the two may overlap."""
+    import torch
+    L, H, D, P, S, T = 4, 8, 128, 16, 4096, 1000
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 121)
+    need = -(-T // P)
+    perm = np.random.default_rng(121).permutation(S // P)[:2 * need].astype(np.int32)
+    px, py = perm[:need].copy(), perm[need:].copy()
+    tx, ty = torch.from_numpy(px).cuda(), torch.from_numpy(py).cuda()
+    staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
+    pool = kv.KVPool(pool_t, P, load_launch=staged, offload_launch=staged, staging_bytes=_staging(2, P, R))
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    with kv.HostBuffer(L * 2 * T * R) as hx, kv.HostBuffer(L * 2 * T * R) as oy:
+        W.fill_np(hx.array, 121, W.LLAMA8B)
+        oy.array[:] = 0
+        torch.cuda.synchronize()
+        for _ in range(3):
+            pool.load([(hx.ptr, T, T, tx.data_ptr())], stream=sa)
+            pool.offload([(oy.ptr, T, T, ty.data_ptr())], stream=sb)
+        sa.synchronize()
+        sb.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, [(hx.array, T, T, px)])
+        e_y = np.zeros(L * 2 * T * R, np.uint8)
+        oracle.offload(pool_np[0].copy(), pool_np[1].copy(), P, [(e_y, T, T, py)])
+        assert np.array_equal(_pool_bytes(pool_t), exp), "load differs from the oracle"
+        assert np.array_equal(oy.array, e_y), "offload differs from the oracle"
+    pool.close()
