@@ -10,8 +10,6 @@ import json
 import math
 import os
 
-import pytest
-
 from oracle.sched import Request, batch_formation, schedule_round
 
 INF = math.inf

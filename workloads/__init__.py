@@ -18,7 +18,7 @@ from __future__ import annotations
 import ctypes
 import dataclasses
 import math
-from typing import List, Optional, Sequence, Tuple
+from typing import List, Sequence, Tuple
 
 import numpy as np
 
