@@ -711,3 +711,39 @@ def test_staged_load_and_offload_concurrently_on_one_handle(kv):
         assert np.array_equal(_pool_bytes(pool_t), exp), "load differs from the oracle"
         assert np.array_equal(oy.array, e_y), "offload differs from the oracle"
     pool.close()
+
+
+@pytest.mark.parametrize("layout,staged", [(0, False), (0, True), (1, False), (2, False)])
+def test_one_byte_elements(kv, layout, staged):
+    """An 8-bit KV cache (e.g. fp8 elements; the copy never looks at values):
+    rows of H * D bytes, against the oracle."""
+    import torch
+    L, H, D, P, S = 2, 8, 128, 16, 4096            # R = 1 KiB; head segments of 128 B
+    R = H * D
+    T, HT = 900, 912
+    rng = np.random.default_rng(131 + layout)
+    pool_np = rng.integers(0, 256, size=(2, L, S, R), dtype=np.uint8)
+    pool_t = torch.from_numpy(pool_np.reshape(2, L, S, H, D).copy()).cuda()
+    pages = rng.permutation(S // P)[:-(-T // P)].astype(np.int32)
+    pt = torch.from_numpy(pages).cuda()
+    launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None
+    pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch, host_layout=layout,
+                     staging_bytes=4 * 4 * 2 * P * R if staged else 0)
+    assert pool.row_bytes == R
+    ora_layout = {0: oracle.TOKEN_MAJOR, 1: oracle.PAGE_FIRST, 2: oracle.HEAD_MAJOR}[layout]
+    nbytes = oracle.host_chunk_bytes(ora_layout, L, HT, R, P)
+    with kv.HostBuffer(nbytes) as hb, kv.HostBuffer(nbytes) as ob:
+        hb.array[:] = rng.integers(0, 256, nbytes, dtype=np.uint8)
+        ob.array[:] = 0x2D
+        pool.load([(hb.ptr, HT, T, pt.data_ptr())])
+        pool.offload([(ob.ptr, HT, T, pt.data_ptr())])
+        torch.cuda.synchronize()
+        pool.check()
+        exp = pool_np.copy()
+        oracle.load_layout(exp[0], exp[1], P, [(hb.array, HT, T, pages)], ora_layout, num_heads=H)
+        got = pool_t.cpu().numpy().reshape(2, L, S, R)
+        assert np.array_equal(got, exp), "load differs from the oracle"
+        exp_out = np.full(nbytes, 0x2D, np.uint8)
+        oracle.offload_layout(exp[0], exp[1], P, [(exp_out, HT, T, pages)], ora_layout, num_heads=H)
+        assert np.array_equal(ob.array, exp_out), "offload differs from the oracle"
+    pool.close()
