@@ -367,6 +367,60 @@ def steady_state(torch, kv, pool, span, host, stream, payload, reps):
     return out
 
 
+def small_context_pipelines(torch, kv, pool, host, T, P, S, used_pages, stream, payload, reps=1000):
+    """Independent small contexts as a server meets them, beside the one-stream
+    steady state: (a) alternating over two streams (the transfer stream and one
+    made before it), each stream loading into its own pages, so one launch's
+    ramp-up overlaps the other's drain; (b) four contexts per batched call.
+    Every context has a host chunk of its own (a repeated chunk would let the
+    GPU serve repeated reads without crossing the link), and the page sets are
+    disjoint, so loads that may run at once never write the same slot."""
+    need = -(-T // P)
+    free = np.setdiff1d(np.arange(S // P, dtype=np.int32), np.asarray(used_pages, np.int32))
+    free = np.random.default_rng(400).permutation(free).astype(np.int32)
+    sets = [np.asarray(used_pages, np.int32)] + [free[i * need:(i + 1) * need] for i in range(len(free) // need)]
+    if len(sets) < 4:
+        return {}
+    tabs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in sets[:4]]
+    chunks = [kv.HostBuffer(payload) for _ in range(4)]
+    early = _PEAK.get("early_streams") or [torch.cuda.Stream()]
+    streams = [stream, early[0]]
+    out = {}
+
+    def timed(issue, n):
+        for _ in range(10):
+            issue(0)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        streams[1].wait_event(e0)
+        for i in range(n):
+            issue(i)
+        joined = torch.cuda.Event()
+        joined.record(streams[1])
+        stream.wait_event(joined)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    try:
+        for c in chunks:
+            c.array[:] = host.array[:payload]
+        ms = timed(lambda i: pool.load([(chunks[i % 2].ptr, T, T, tabs[i % 2].data_ptr())], stream=streams[i % 2]),
+                   reps)
+        out["two_streams_load_gbps"] = round(reps * payload / (ms * 1e-3) / GB, 3)
+        batch = [(c.ptr, T, T, t.data_ptr()) for c, t in zip(chunks, tabs)]
+        calls = reps // 4
+        ms = timed(lambda i: pool.load(batch, stream=stream), calls)
+        out["batched4_load_gbps"] = round(calls * 4 * payload / (ms * 1e-3) / GB, 3)
+        pool.check()
+    finally:
+        for c in chunks:
+            c.free()
+    return out
+
+
 def base_result(args, value, ms_per_step, workload, extra_config):
     cfg = {"workload": workload}
     cfg.update(extra_config)
@@ -1456,8 +1510,15 @@ def run_single(args, torch, kv, W, k):
     steady = None
     if k == 1:
         steady = steady_state(torch, kv, pool, span_in, host, stream, payload, reps=1000)
+        steady.update(small_context_pipelines(torch, kv, pool, host, T, P, S, pages, stream, payload))
+        if peak:   # the target is set against the steady state (a single 2 MiB shot is latency-bound)
+            for key in ("load", "memcpy", "two_streams_load", "batched4_load"):
+                if f"{key}_gbps" in steady:
+                    steady[f"{key}_frac_of_h2d_peak"] = round(steady[f"{key}_gbps"] / peak["h2d"], 4)
         log(f"steady state over 1000 loads: {steady['load_gbps']:.2f} GB/s, single shot "
-            f"{steady['single_shot_us']:.1f} us; same-size memcpy {steady['memcpy_gbps']:.2f} GB/s")
+            f"{steady['single_shot_us']:.1f} us; same-size memcpy {steady['memcpy_gbps']:.2f} GB/s; "
+            f"independent contexts on two streams {steady.get('two_streams_load_gbps')} GB/s, "
+            f"four per batched call {steady.get('batched4_load_gbps')} GB/s")
 
     default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host
                           or args.no_lds or args.staged or args.host_layout != "token")
