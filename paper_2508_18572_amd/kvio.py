@@ -9,7 +9,9 @@ this module raises.
 Names follow the C ABI (kvio_load, kvio_offload, kvio_load_layer, ...).
 Pointers are Python ints (``tensor.data_ptr()``); streams are
 ``torch.cuda.Stream`` objects, raw ``hipStream_t`` ints, or None (the default
-stream); events are ``torch.cuda.Event`` objects or raw ints.
+stream); events are ``torch.cuda.Event`` objects or raw ints (a torch event
+that was never recorded has no HIP event yet; it is recorded once on the
+current stream first, then by the library after its launch).
 """
 from __future__ import annotations
 
@@ -172,7 +174,12 @@ def _event(e) -> Optional[int]:
         return None
     if isinstance(e, int):
         return e or None
-    return e.cuda_event or None
+    if not e.cuda_event:
+        # torch creates the HIP event at its first record; record it once (on
+        # the current stream) so that there is a handle for the library to
+        # record after its launch
+        e.record()
+    return e.cuda_event
 
 
 SpanLike = Union[kvio_span, Tuple[int, int, int, int]]

@@ -747,3 +747,34 @@ def test_one_byte_elements(kv, layout, staged):
         oracle.offload_layout(exp[0], exp[1], P, [(exp_out, HT, T, pages)], ora_layout, num_heads=H)
         assert np.array_equal(ob.array, exp_out), "offload differs from the oracle"
     pool.close()
+
+
+def test_load_layer_records_a_fresh_torch_event(kv):
+    """`done` may be a torch event that was never recorded (torch creates its
+    HIP event lazily): the binding materialises it and the library records it
+    after the launch, so waiting on it alone (no device-wide synchronisation)
+    leaves the layer fully loaded.  The layer is 64 MiB, about a millisecond
+    of transfer, so an event recorded before the launch would expose rows
+    still in flight."""
+    import torch
+    L, H, D, P, S, T = 2, 8, 128, 16, 32768, 16384
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 141)
+    pages = np.random.default_rng(141).permutation(S // P)[:T // P].astype(np.int32)
+    pt = torch.from_numpy(pages).cuda()
+    pool = kv.KVPool(pool_t, P)
+    s = torch.cuda.Stream()
+    with kv.HostBuffer(L * 2 * T * R) as hb:
+        W.fill_np(hb.array, 141, W.LLAMA8B)
+        torch.cuda.synchronize()
+        ev = torch.cuda.Event()
+        assert ev.cuda_event == 0
+        pool.load_layer([(hb.ptr, T, T, pt.data_ptr())], 1, stream=s, done=ev)
+        assert ev.cuda_event != 0
+        ev.synchronize()
+        got = pool_t[:, 1].cpu().numpy().view(np.uint8).reshape(2, S, R)   # current stream: idle
+        exp = pool_np.copy()
+        oracle.load(exp[0], exp[1], P, [(hb.array, T, T, pages)], 1, 2)
+        assert np.array_equal(got, exp[:, 1]), "layer 1 incomplete after waiting on its event"
+    torch.cuda.synchronize()
+    pool.close()
