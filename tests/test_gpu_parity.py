@@ -382,10 +382,11 @@ def test_validation_errors(kv):
         plain = np.zeros(L * 2 * T * R, np.uint8)                            # plain malloc memory
         cases.append(([(plain.ctypes.data, T, T, pt.data_ptr())], 0, L, kv.KVIO_ENOTMAPPED))
         for spans, l0, l1, code in cases:
-            with pytest.raises(kv.KvioError) as e:
-                pool.load(spans, l0, l1)
-            assert e.value.status == code, (spans, e.value)
-            assert kv.kvio_last_error() == "" or True
+            for call in (pool.load, pool.offload):
+                with pytest.raises(kv.KvioError) as e:
+                    call(spans, l0, l1)
+                assert e.value.status == code, (call, spans, e.value)
+                assert e.value.detail and kv.kvio_last_error() == e.value.detail
         torch.cuda.synchronize()
         assert np.array_equal(_pool_bytes(pool_t), pool_np)
     with pytest.raises(kv.KvioError) as e:
