@@ -77,3 +77,24 @@ def test_pins_catch_mutant(tmp_path, name, old, new, occ):
                         os.path.join(ROOT, "tests", "test_oracle_layouts.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+# Mutants of the copy's arithmetic (not of its input validation, which the
+# property tests never exercise): the hypothesis-drawn properties alone must
+# catch each of them too.
+VALIDATION_MUTANTS = {"no_duplicate_check", "layer_end_inclusive_check"}
+
+
+@pytest.mark.parametrize("name,old,new,occ", [m for m in MUTANTS if m[0] not in VALIDATION_MUTANTS],
+                         ids=[m[0] for m in MUTANTS if m[0] not in VALIDATION_MUTANTS])
+def test_properties_catch_arithmetic_mutant(tmp_path, name, old, new, occ):
+    mutated = open(SRC).read().replace(old, new)
+    c = tmp_path / "mutant.c"
+    c.write_text(mutated)
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-std=c99", "-O1", "-fPIC", "-shared", str(c), "-o", str(lib)], check=True)
+    env = dict(os.environ, KVO_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_properties.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0, f"mutant {name} survived the property tests:\n{r.stdout[-2000:]}"
