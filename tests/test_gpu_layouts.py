@@ -84,6 +84,7 @@ SHAPES = [
     (2, 128, 128, 1, 64, [(10, 12)]),                   # R = 32 KiB: wider than a step
     (1, 4, 64, 100, 1000, [(250, 300), (100, 100)]),    # P = 100 (no shift), page > one tile
     (1, 1, 8, 128, 128, [(100, 128)]),                  # a one-page pool, R = 16 B
+    (40, 2, 8, 4, 64, [(30, 32)]),                      # 80 layer pointers: more than one per lane
 ]
 
 

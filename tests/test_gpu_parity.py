@@ -109,6 +109,7 @@ def run_case(kv, L, H, D, P, S, spans, l0=0, l1=None, launch=None, seed=0, shape
     (1, 1, 8, 128, 128, [(100, 128)]),                    # a one-page pool, page > one tile
     (2, 8, 128, 256, 1024, [(700, 768)]),                 # P = 256: pages span several tiles
     (1, 4, 64, 100, 1000, [(250, 300), (100, 100)]),      # P = 100 (no shift), > one tile
+    (40, 1, 8, 4, 64, [(30, 33), (9, 9)]),                # 80 layer pointers: more than one per lane
 ])
 def test_parity_shapes(kv, L, H, D, P, S, spans):
     run_case(kv, L, H, D, P, S, spans, seed=L * 31 + P)
