@@ -270,6 +270,48 @@ __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, ui
     }
 }
 
+// The first tile of a load wave: its host reads are issued before anything
+// else (their addresses come from the kernel arguments alone), and the pool
+// layer and the slots are resolved while they are in flight, which shortens
+// the start of every launch.  Chunks that do not move read the tile's first
+// host row instead (in bounds, discarded).  Later tiles run through the step
+// functions above.
+template <int U, bool NT, bool WIDE, int HL>
+__device__ __forceinline__ void first_load_step(const CopyArgs &a, const SpanArg &sp, const TileLoc &loc,
+                                                uint8_t *host, uint8_t *&pool, int &slot, int64_t hoff,
+                                                int nvec, int lane) {
+    const int64_t R = a.row_bytes;
+    const int V = a.vec_per_row;
+    const uint32_t lane_off = static_cast<uint32_t>(lane) * 16u;
+    int row[U], col[U];
+    int64_t host_off[U];
+    u32x4 buf[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+        const int j = k * 64 + (WIDE ? 0 : lane);          // WIDE: chunk k's first vector (uniform)
+        row[k] = row_of(a, j);
+        col[k] = j - row[k] * V;
+        if constexpr (HL == kHostPageFirst)
+            host_off[k] = (WIDE ? readlane64(hoff, row[k] & 63) : static_cast<int64_t>(__shfl(
+                                                                       static_cast<long long>(hoff), row[k] & 63))) +
+                          col[k] * 16;
+        else
+            host_off[k] = static_cast<int64_t>(j) * 16;
+        const bool valid = WIDE ? (k * 64 < nvec) : (j < nvec);
+        buf[k] = load16<NT>(valid ? host + host_off[k] + (WIDE ? lane_off : 0u) : host);
+    }
+    pool = a.layers[loc.kv * a.num_layers + loc.layer];
+    slot = lane_slot(a, sp, loc.t0, loc.nrows, lane);
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+        const int j = k * 64 + (WIDE ? 0 : lane);
+        const bool valid = WIDE ? (k * 64 < nvec) : (j < nvec);
+        const int s = WIDE ? __builtin_amdgcn_readlane(slot, row[k] & 63) : __shfl(slot, row[k] & 63);
+        if (valid && s >= 0)
+            store16<NT>(pool + static_cast<int64_t>(s) * R + col[k] * 16 + (WIDE ? lane_off : 0u), buf[k]);
+    }
+}
+
 // DIR: kLoad (host chunk -> pool) or kOffload (pool -> host chunk).
 // U: 16-byte vectors per lane per step (one step = U KiB per wave).
 // WIDE: R is a multiple of 1 KiB (see step_wide).  HL: host layout.
@@ -287,12 +329,12 @@ __global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBo
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * waves_per_wg;
     const uint32_t lane_off = static_cast<uint32_t>(lane) * 16u;
 
+    int64_t g = static_cast<int64_t>(blockIdx.x) * waves_per_wg + wave_in_wg;
+    bool first = DIR == kLoad;
 #pragma unroll 1
-    for (int64_t g = static_cast<int64_t>(blockIdx.x) * waves_per_wg + wave_in_wg;
-         g < a.total_tiles; g += nwaves) {
+    for (; g < a.total_tiles; g += nwaves) {
         const TileLoc loc = locate(a, g);
         const SpanArg &sp = a.spans[loc.span];
-        uint8_t *pool = a.layers[loc.kv * a.num_layers + loc.layer];
         uint8_t *host = const_cast<uint8_t *>(sp.host);
         int64_t hoff = 0;
         if constexpr (HL == kHostPageFirst) {
@@ -301,10 +343,20 @@ __global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBo
             // First byte of the tile's rows (layer-major chunk, K then V).
             host += ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * sp.host_tokens + loc.t0) * a.row_bytes;
         }
-        const int slot = lane_slot(a, sp, loc.t0, loc.nrows, lane);
         const int nvec = loc.nrows * a.vec_per_row;
+        uint8_t *pool;
+        int slot;
+        int base = 0;
+        if (first) {
+            first = false;
+            first_load_step<U, NT, WIDE, HL>(a, sp, loc, host, pool, slot, hoff, nvec, lane);
+            base = 64 * U;
+        } else {
+            pool = a.layers[loc.kv * a.num_layers + loc.layer];
+            slot = lane_slot(a, sp, loc.t0, loc.nrows, lane);
+        }
 #pragma unroll 1
-        for (int base = 0; base < nvec; base += 64 * U) {
+        for (; base < nvec; base += 64 * U) {
             if constexpr (WIDE) {
                 step_wide<DIR, U, NT, HL>(a, host, pool, slot, hoff, base, nvec, lane_off);
             } else {
