@@ -823,27 +823,54 @@ def run_interference(args, torch, kv, W):
         "decode_hbm": lambda: torch.sum(kvbuf, dim=(0,), dtype=torch.float32, out=red),
     }
 
-    def alone(fn, n=20):
+    def alone(fn, n=20, stream=None):
+        stream = comp if stream is None else stream
         ts = []
         for _ in range(n):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(comp)
-            with torch.cuda.stream(comp):
+            a.record(stream)
+            with torch.cuda.stream(stream):
                 fn()
-            b.record(comp)
+            b.record(stream)
             ts.append((a, b))
         torch.cuda.synchronize()
         return statistics.median(x.elapsed_time(y) for x, y in ts)
 
-    def load_alone(pool):
-        pool.load(span, stream=io)
+    def load_alone(pool, stream=None):
+        stream = io if stream is None else stream
+        pool.load(span, stream=stream)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(io)
-        pool.load(span, stream=io)
-        b.record(io)
+        a.record(stream)
+        pool.load(span, stream=stream)
+        b.record(stream)
         torch.cuda.synchronize()
         return a.elapsed_time(b)
+
+    def corun(pool, fn, n_iter, io_s, comp_s):
+        """The co-runner loops on comp_s while one load runs on io_s: load GB/s
+        and the median co-runner iteration inside the load's window."""
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(comp_s)
+        marks = []
+        with torch.cuda.stream(comp_s):
+            for _ in range(n_iter):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(comp_s)
+                fn()
+                b.record(comp_s)
+                marks.append((a, b))
+        io_s.wait_event(marks[5][0])                        # the co-runner is already running
+        l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        l0.record(io_s)
+        pool.load(span, stream=io_s)
+        l1.record(io_s)
+        torch.cuda.synchronize()
+        t0, t1 = start.elapsed_time(l0), start.elapsed_time(l1)
+        inside = [x.elapsed_time(y) for x, y in marks
+                  if start.elapsed_time(x) >= t0 and start.elapsed_time(y) <= t1]
+        return round(nb / ((t1 - t0) * 1e-3) / GB, 3), (round(statistics.median(inside), 4) if inside else None)
 
     quotas = [(1, 1024), (2, 1024), (4, 1024), (2, 256), (4, 256), (8, 256), (16, 256), (32, 256),
               (64, 256), (128, 256), (32, 64), (64, 64), (128, 64), (256, 64), (64, 128), (128, 128),
@@ -863,29 +890,37 @@ def run_interference(args, torch, kv, W):
                "load_gbps_alone": round(nb / (load_alone(pool) * 1e-3) / GB, 3)}
         for name, fn in corunners.items():
             n_iter = int(200 / base[name]) + 20            # enough to outlast the load
-            torch.cuda.synchronize()
-            start = torch.cuda.Event(enable_timing=True)
-            start.record(comp)
-            marks = []
-            with torch.cuda.stream(comp):
-                for _ in range(n_iter):
-                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    a.record(comp)
-                    fn()
-                    b.record(comp)
-                    marks.append((a, b))
-            io.wait_event(marks[5][0])                      # the co-runner is already running
-            l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            l0.record(io)
-            pool.load(span, stream=io)
-            l1.record(io)
-            torch.cuda.synchronize()
-            t0, t1 = start.elapsed_time(l0), start.elapsed_time(l1)
-            inside = [x.elapsed_time(y) for x, y in marks
-                      if start.elapsed_time(x) >= t0 and start.elapsed_time(y) <= t1]
-            row[f"load_gbps_with_{name}"] = round(nb / ((t1 - t0) * 1e-3) / GB, 3)
-            row[f"{name}_ms_corun"] = round(statistics.median(inside), 4) if inside else None
+            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"] = corun(pool, fn, n_iter, io, comp)
         pool.close()
+        rows.append(row)
+    # CU partitions: the load (default shape, 16 workgroups) on a stream masked
+    # to 16 CUs and the co-runner on a stream masked to the other CUs, so no CU
+    # holds both; the first 16 CUs, and every 16th CU.
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    for label, io_cus in (("cu_mask_first_16", list(range(16))),
+                          ("cu_mask_every_16th", list(range(0, n_cu, n_cu // 16))[:16])):
+        try:
+            io_m = kv.Stream(io_cus)
+        except kv.KvioError as e:
+            log(f"{label}: masked stream refused ({e.detail})")
+            continue
+        try:
+            comp_m = kv.Stream([c for c in range(n_cu) if c not in io_cus])
+        except kv.KvioError as e:
+            log(f"{label}: masked stream refused ({e.detail})")
+            io_m.close()
+            continue
+        pool = kv.KVPool(pool_t, P)
+        row = {"workgroups": label, "threads": 256, "waves": 64,
+               "load_gbps_alone": round(nb / (load_alone(pool, io_m.torch) * 1e-3) / GB, 3)}
+        for name, fn in corunners.items():
+            row[f"{name}_ms_alone_on_{n_cu - 16}_cus"] = round(alone(fn, stream=comp_m.torch), 4)
+            n_iter = int(200 / base[name]) + 20
+            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"] = corun(pool, fn, n_iter, io_m.torch,
+                                                                          comp_m.torch)
+        pool.close()
+        comp_m.close()
+        io_m.close()
         rows.append(row)
     # the baseline: the faster of the co-runner alone before and after the sweep
     after = {name: alone(fn) for name, fn in corunners.items()}

@@ -34,7 +34,10 @@
  *     crosses the ABI.  On error kvio_last_error() holds a thread-local text.
  *   - Transfers are asynchronous on the given stream (NULL = the default
  *     stream); completion follows stream order.  Validation errors are
- *     reported synchronously and enqueue nothing.  The transfer calls enqueue
+ *     reported synchronously and enqueue nothing.  A HIP call that fails
+ *     inside the library is reported by the status and kvio_last_error();
+ *     the runtime's per-thread last error is cleared, so the caller's next
+ *     HIP call does not report it again.  The transfer calls enqueue
  *     no memset and allocate nothing, so they can be captured into a HIP
  *     graph (a staged call forks its side stream from the captured stream and
  *     joins it back through events).

@@ -36,6 +36,9 @@ kvio_status fail(kvio_status st, const char *fmt, ...) {
 }
 
 kvio_status fail_hip(hipError_t e, const char *what) {
+    // The status and the text carry the error; clear the runtime's per-thread
+    // last error so the caller's next, unrelated HIP call does not report it.
+    (void)hipGetLastError();
     return fail(KVIO_EHIP, "%s: %s (%s)", what, hipGetErrorString(e), hipGetErrorName(e));
 }
 
@@ -289,6 +292,7 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
         if (staged[dir]) e = create_staging(p, dir, int64_t(kStageSlots) * slot_bytes);
     if (e != hipSuccess) {
         (void)release_pool(p);
+        (void)hipGetLastError();
         return e == hipErrorOutOfMemory ? fail(KVIO_ENOMEM, "kvio_pool_create: device allocation failed")
                                         : fail_hip(e, "kvio_pool_create");
     }

@@ -780,3 +780,22 @@ def test_load_layer_records_a_fresh_torch_event(kv):
         assert np.array_equal(got, exp[:, 1]), "layer 1 incomplete after waiting on its event"
     torch.cuda.synchronize()
     pool.close()
+
+
+def test_a_failed_runtime_call_does_not_leak_into_the_callers_next_call(kv):
+    """A HIP failure inside the library is reported by its status only: the
+    runtime's per-thread last error is cleared, so torch's next kernel launch
+    (which checks it) still succeeds.  Forced from the host: pinned memory far
+    beyond what the machine holds."""
+    import torch
+    pool_t = torch.zeros((2, 2, 1024, 8, 128), dtype=torch.bfloat16, device="cuda")
+    staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
+    with pytest.raises(kv.KvioError) as e:          # 1 PiB of HBM staging: the device allocation fails
+        kv.KVPool(pool_t, 16, load_launch=staged, staging_bytes=1 << 50)
+    assert e.value.status == kv.KVIO_ENOMEM
+    x = torch.ones(1 << 20, device="cuda")          # torch checks the last error after its launch
+    assert float(x.sum().item()) == float(1 << 20)
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_host_alloc(1 << 52)                 # 4 PiB of pinned host memory
+    assert e.value.status in (kv.KVIO_ENOMEM, kv.KVIO_EHIP)
+    assert float(torch.ones(1 << 10, device="cuda").sum().item()) == float(1 << 10)
