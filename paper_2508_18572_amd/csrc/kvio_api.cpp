@@ -424,10 +424,7 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
         }
         lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
     }
-    const kvio::Shape &def = dir == kvio::kOffload                    ? kvio::kDefaultOffload
-                             : p->host_layout == KVIO_HOST_HEAD_MAJOR ? kvio::kDefaultHeadMajorLoad
-                                                                      : kvio::kDefaultLoad;
-    kvio::Shape shape = resolve(lc, def);
+    kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);
     // LDS staging of a head-major tile needs the whole tile (>= one row) in the
     // wave's U KiB slice.
     if (p->host_layout == KVIO_HOST_HEAD_MAJOR && p->row_bytes > int64_t(shape.tile_kib) * 1024)

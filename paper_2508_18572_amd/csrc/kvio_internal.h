@@ -70,9 +70,6 @@ struct Shape {
 constexpr int kDefaultThreads = 256;
 constexpr Shape kDefaultLoad = {16, kDefaultThreads, 4, true, true};
 constexpr Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
-// Head-major chunks load through the LDS transpose with 8 KiB steps: 57.4
-// GB/s on the same workload in every run, against 56.3-57.3 at 4 KiB.
-constexpr Shape kDefaultHeadMajorLoad = {16, kDefaultThreads, 8, true, true};
 // Staged transfers: the scatter / gather between the HBM staging buffer and
 // the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at
 // page size 1 in 1.75 ms, 2.4 TB/s of payload).
