@@ -135,7 +135,11 @@ typedef struct kvio_launch {
     int32_t flags;        /* KVIO_LAUNCH_* bits                                              */
 } kvio_launch;
 
-/* Describes caller-owned device memory; copied by kvio_pool_create. */
+/* Describes caller-owned device memory; copied by kvio_pool_create.  The
+ * memory is the GPU's paged KV cache (Sec. 2.2: KV states kept in fixed-size
+ * pages of token slots, one pool per layer), addressed through a page table
+ * that the caller's cache index maintains (Sec. 4.1: the HiRadixTree maps
+ * cached tokens to pool indices; Sec. 4.2.1: the pool is layer-first). */
 typedef struct kvio_pool_desc {
     int32_t num_layers;       /* L >= 1                                                  */
     int32_t num_kv_heads;     /* H >= 1                                                  */
@@ -156,7 +160,12 @@ typedef struct kvio_pool_desc {
 
 typedef struct kvio_pool *kvio_pool_t;
 
-/* One cached context (one "span" of a batched transfer). */
+/* One cached context (one "span" of a batched transfer): its contiguous host
+ * chunk (Sec. 4.2.1: the host keeps each context in one transfer-friendly
+ * chunk) and the page table that places its tokens in the pool (Sec. 2.2 paged
+ * KV; Sec. 4.1: the cache index resolves a context to pool pages).  A batched
+ * call moves several contexts at once, as the scheduler issues one load per
+ * batch (Sec. 4.3.2). */
 typedef struct kvio_span {
     void *host;               /* pinned, device-mapped host chunk (or device memory),
                                  16-byte aligned, L * 2 * host_tokens * R bytes        */
@@ -169,7 +178,8 @@ typedef struct kvio_span {
  * consecutive launches on the same stream. */
 #define KVIO_MAX_SPANS_PER_LAUNCH 64
 
-/* Create a pool handle on the current device.  Checks that every layer
+/* Create a pool handle on the current device (Sec. 2.2 / Sec. 4.1: the paged
+ * pool and its page addressing that every transfer names).  Checks that every layer
  * pointer is device memory of at least S * R bytes and 16-byte aligned
  * (KVIO_EINVAL / KVIO_EALIGN), then allocates the handle (KVIO_ENOMEM /
  * KVIO_EHIP).  *out is set only on success. */
@@ -202,7 +212,8 @@ kvio_status kvio_offload(kvio_pool_t pool, const kvio_span *spans, int32_t n_spa
 kvio_status kvio_load_layer(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
                             int32_t layer, hipStream_t stream, hipEvent_t done);
 
-/* Synchronise the device, then report and clear the device error record:
+/* The library's own error reporting; no passage of the paper defines it.
+ * Synchronise the device, then report and clear the device error record:
  * KVIO_ERANGE (with the span and context page in kvio_last_error) if an
  * earlier transfer met an out-of-range page index, else KVIO_OK. */
 kvio_status kvio_check(kvio_pool_t pool);
@@ -331,7 +342,8 @@ kvio_status kvio_disk_prefetch_finish(kvio_prefetch_t job, int32_t cancel, uint8
  *      is loaded once).  Then, while the batch is not full, requests are taken
  *      in queue order: one that would make the batch loading-bound --
  *      aggregated load tokens > loading_bound_ratio * aggregated compute
- *      tokens, compared in double precision -- is deprioritized, otherwise it
+ *      tokens, decided exactly on the integer token sums and the ratio's
+ *      binary value (no rounding) -- is deprioritized, otherwise it
  *      joins and pulls in its own bundle hits.  Deprioritized requests then
  *      fill any room left, in their original order.
  * "Full" means the batch's compute tokens reached max_tokens or its size

@@ -13,15 +13,84 @@
 
 namespace {
 
-// Token sums are kept in 128 bits: n requests of up to 2^63 tokens each
-// cannot overflow them, and the loading-bound test converts them to double
-// (rounding to nearest) as the definition does.
+// Token sums are kept in 128 bits: n < 2^31 requests of fewer than 2^63 tokens
+// each sum to less than 2^94, so they cannot overflow.
 struct Batch {
-    __int128 load = 0;
-    __int128 compute = 0;
+    unsigned __int128 load = 0;
+    unsigned __int128 compute = 0;
     int32_t count = 0;
     std::unordered_set<int64_t> contexts;
 };
+
+// Unsigned 256-bit integer, four 64-bit limbs, least significant first: wide
+// enough for a token sum (< 2^94) times the 53-bit significand of the ratio.
+struct U256 {
+    uint64_t w[4] = {0, 0, 0, 0};
+};
+
+U256 from_u128(unsigned __int128 v) {
+    U256 r;
+    r.w[0] = uint64_t(v);
+    r.w[1] = uint64_t(v >> 64);
+    return r;
+}
+
+U256 mul_u128_u64(unsigned __int128 a, uint64_t b) {
+    const unsigned __int128 lo = (unsigned __int128)uint64_t(a) * b;
+    const unsigned __int128 hi = (unsigned __int128)uint64_t(a >> 64) * b + (lo >> 64);
+    U256 r;
+    r.w[0] = uint64_t(lo);
+    r.w[1] = uint64_t(hi);
+    r.w[2] = uint64_t(hi >> 64);
+    return r;
+}
+
+int bit_length(const U256 &v) {
+    for (int i = 3; i >= 0; --i)
+        if (v.w[i] != 0) return 64 * i + 64 - __builtin_clzll(v.w[i]);
+    return 0;
+}
+
+// v * 2^s; the caller keeps the result below 2^256.
+U256 shl(const U256 &v, int s) {
+    U256 r;
+    const int limbs = s / 64, bits = s % 64;
+    for (int i = 3; i >= limbs; --i) {
+        uint64_t x = v.w[i - limbs] << bits;
+        if (bits != 0 && i - limbs - 1 >= 0) x |= v.w[i - limbs - 1] >> (64 - bits);
+        r.w[i] = x;
+    }
+    return r;
+}
+
+int compare(const U256 &a, const U256 &b) {
+    for (int i = 3; i >= 0; --i)
+        if (a.w[i] != b.w[i]) return a.w[i] < b.w[i] ? -1 : 1;
+    return 0;
+}
+
+// Sec. 4.3.2: the batch is loading-bound when the ratio of its aggregated load
+// to its aggregated compute exceeds the threshold.  Decided exactly as
+// load > ratio * compute on the integer sums and the ratio's exact binary
+// value (ratio = m * 2^k with an integer significand m < 2^53), so the
+// outcome never depends on rounding: no compute and some load is
+// loading-bound; an infinite ratio never is.
+bool exceeds_ratio(unsigned __int128 load, unsigned __int128 compute, double ratio) {
+    if (isinf(ratio)) return false;
+    if (compute == 0) return load != 0;
+    if (load == 0) return false;
+    int e = 0;
+    const double f = frexp(ratio, &e);                  // ratio = f * 2^e, f in [0.5, 1)
+    const uint64_t m = uint64_t(ldexp(f, 53));          // exact: ratio = m * 2^(e - 53)
+    const int k = e - 53;
+    // compare A * 2^a with B * 2^b: A = load, B = m * compute
+    const U256 A = from_u128(load), B = mul_u128_u64(compute, m);
+    const int a = k < 0 ? -k : 0, b = k > 0 ? k : 0;
+    const int la = bit_length(A) + a, lb = bit_length(B) + b;
+    if (la != lb) return la > lb;
+    // equal bit lengths: the shift that aligns them keeps both below 2^256
+    return a >= b ? compare(shl(A, a - b), B) > 0 : compare(A, shl(B, b - a)) > 0;
+}
 
 }  // namespace
 
@@ -62,15 +131,17 @@ extern "C" kvio_status kvio_schedule_round(const kvio_request *queue, int32_t n,
     auto is_bundle_hit = [&](int32_t i) {
         return queue[i].context >= 0 && B.contexts.count(queue[i].context) != 0;
     };
-    auto is_full = [&]() { return B.compute >= policy->max_tokens || B.count >= policy->max_requests; };
+    auto is_full = [&]() {
+        return B.compute >= uint64_t(policy->max_tokens) || B.count >= policy->max_requests;
+    };
     auto loading_bound = [&](int32_t i) {
-        const __int128 load = B.load + (is_bundle_hit(i) ? 0 : queue[i].load_tokens);
-        const __int128 compute = B.compute + queue[i].compute_tokens;
-        return double(load) > ratio * double(compute);
+        const unsigned __int128 load = B.load + uint64_t(is_bundle_hit(i) ? 0 : queue[i].load_tokens);
+        const unsigned __int128 compute = B.compute + uint64_t(queue[i].compute_tokens);
+        return exceeds_ratio(load, compute, ratio);
     };
     auto add = [&](int32_t i) {
-        if (!is_bundle_hit(i)) B.load += queue[i].load_tokens;
-        B.compute += queue[i].compute_tokens;
+        if (!is_bundle_hit(i)) B.load += uint64_t(queue[i].load_tokens);
+        B.compute += uint64_t(queue[i].compute_tokens);
         B.count += 1;
         if (queue[i].context >= 0) B.contexts.insert(queue[i].context);
         queued[size_t(i)] = 0;

@@ -15,28 +15,31 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 # (module, name, original text, replacement)
 MUTANTS = [
     ("sched", "bundle_hits_never_join",
-     "        if batch.is_bundle_hit(queue[i]):\n", "        if False:\n"),
+     "if state[pos] == _WAITING and c is not None and c in contexts_in_batch:", "if False:"),
     ("sched", "loading_bound_flipped",
-     "return float(load) > float(self.ratio) * float(compute)",
-     "return float(load) < float(self.ratio) * float(compute)"),
+     "return Fraction(load) > Fraction(ratio) * compute", "return Fraction(load) < Fraction(ratio) * compute"),
+    ("sched", "loading_bound_rounded_to_double",
+     "return Fraction(load) > Fraction(ratio) * compute", "return float(load) > ratio * float(compute)"),
     ("sched", "bundle_hit_load_counted",
-     "return 0 if self.is_bundle_hit(r) else r.load_tokens", "return r.load_tokens"),
+     'return totals["load"] + (0 if shared else r.load_tokens)', 'return totals["load"] + r.load_tokens'),
     ("sched", "deprioritized_never_fill",
-     "    for r in deprioritized:\n", "    for r in deprioritized[:0]:\n"),
+     "    for pos in range(n):             # set-aside", "    for pos in range(0):             # set-aside"),
     ("sched", "full_only_past_budget",
-     "return self.compute >= self.max_tokens or", "return self.compute > self.max_tokens or"),
+     'return totals["compute"] < max_tokens and', 'return totals["compute"] <= max_tokens and'),
     ("sched", "deferral_at_threshold",
-     "deferred = [r for r in queue if r.transient_matches > delay_hit_threshold]\n"
+     "deferred = [r.rid for r in queue if r.transient_matches > delay_hit_threshold]\n"
      "    eligible = [r for r in queue if r.transient_matches <= delay_hit_threshold]",
-     "deferred = [r for r in queue if r.transient_matches >= delay_hit_threshold]\n"
+     "deferred = [r.rid for r in queue if r.transient_matches >= delay_hit_threshold]\n"
      "    eligible = [r for r in queue if r.transient_matches < delay_hit_threshold]"),
     ("sched", "deferred_go_last",
-     "return batch, [r.rid for r in deferred] + rest", "return batch, rest + [r.rid for r in deferred]"),
+     "return batch, deferred + rest", "return batch, rest + deferred"),
     ("sched", "head_checked_like_the_rest",
-     "    batch.add(q.pop(0))\n    add_bundle_hit(q, batch)\n", ""),
+     "    enter(0)                         # the head of the queue always starts the batch\n"
+     "    enter_bundle_hits()\n    for pos in range(1, n):",
+     "    for pos in range(0, n):"),
     ("sched", "rest_reversed",
-     "rest = sorted((r for r in queue if r.rid not in taken), key=lambda r: order[r.rid])",
-     "rest = sorted((r for r in queue if r.rid not in taken), key=lambda r: -order[r.rid])"),
+     "rest = [queue[p].rid for p in range(n) if state[p] != _IN_BATCH]",
+     "rest = [queue[p].rid for p in reversed(range(n)) if state[p] != _IN_BATCH]"),
     ("disk", "page_first_layer_page_swapped",
      "return (((page * num_layers + layer) * 2 + kv) * page_size + in_page) * row_bytes",
      "return (((layer * num_layers + page) * 2 + kv) * page_size + in_page) * row_bytes"),

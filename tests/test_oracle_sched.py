@@ -1,8 +1,8 @@
-"""Pins of the batch-formation oracle (Strata Sec. 4.3, Algorithm 1).
+"""Pins of the batch-formation oracle (Strata Sec. 4.3.1 and Sec. 4.3.2).
 
 The paper's Figure 7 narrative gives the worked example: with C and D0 both
 needing large context loads, FIFO would batch (C, D0) and stall on loading;
-Algorithm 1 forms (C, F) so C's load overlaps F's compute, and D0 with D1 —
+balanced batch formation forms (C, F) so C's load overlaps F's compute, and D0 with D1 —
 which share one context — form a bundle-hit batch next.  The numbers below
 are chosen so that exactly those decisions follow from a ratio of 100.
 """
@@ -159,3 +159,24 @@ def test_shared_context_loads_once():
          Request(3, 0, 5)]
     batch, rest = batch_formation(q, max_tokens=10**6, max_requests=3)
     assert batch == [0, 1, 2] and rest == [3]
+
+
+def test_ratio_test_is_exact_past_double_precision():
+    # Sec. 4.3.2: loading-bound when load / compute exceeds the ratio.  With
+    # compute 2^60 and load 2^60 + 1 the ratio is above 1 by 2^-60, which a
+    # double cannot see (2^60 + 1 rounds to 2^60): request 1 is set aside and
+    # fills the room only after request 2.
+    big = 2**60
+    q = [Request(0, 0, big), Request(1, big + 1, 0), Request(2, 0, 1)]
+    assert batch_formation(q, max_tokens=2**62, max_requests=8, ratio=1.0) == ([0, 2, 1], [])
+    # exactly at the ratio is not above it: request 1 joins in queue order
+    q = [Request(0, 0, big), Request(1, big, 0), Request(2, 0, 1)]
+    assert batch_formation(q, max_tokens=2**62, max_requests=8, ratio=1.0) == ([0, 1, 2], [])
+
+
+def test_no_compute_is_loading_bound_once_anything_loads():
+    # load / 0 exceeds any finite ratio; 0 / 0 does not (nothing to load)
+    q = [Request(0, 0, 0), Request(1, 5, 0), Request(2, 0, 0)]
+    assert batch_formation(q, max_tokens=10, max_requests=8, ratio=10**9) == ([0, 2, 1], [])
+    # an infinite ratio is plain FIFO
+    assert batch_formation(q, max_tokens=10, max_requests=8, ratio=INF) == ([0, 1, 2], [])
