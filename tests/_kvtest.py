@@ -88,3 +88,124 @@ def untouched_rows_hold_sentinel(pool_t, touched: np.ndarray, layers, layer_rang
                                          f"{bad_touched} touched rows still sentinel")
             elif not bool(is_sent.all()):
                 raise AssertionError(f"kv {kv} layer {l} outside the layer range was written")
+
+
+_libc.memset.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t]
+_libc.memset.restype = ctypes.c_void_p
+
+
+def _for_each_slab(pool_t, check, workers):
+    """Copy every (K|V, layer) slab of the GPU pool into pinned host memory and
+    run check(kv, layer, image) on it, `workers` slabs at a time (the copies
+    and the oracle's C calls run without the interpreter lock).  `image` is an
+    (S, R) uint8 view valid during the call.  Returns the failure messages."""
+    import torch
+
+    import paper_2508_18572_amd as kvmod
+    _, L, S = pool_t.shape[:3]
+    R = pool_t[0, 0, 0].numel() * pool_t.element_size()
+    pool_b = pool_t.view(torch.uint8).view(2, L, S, R)
+    planes = [(kv, l) for l in range(L) for kv in range(2)]
+    torch.cuda.synchronize()
+
+    def work(w):
+        errors = []
+        with kvmod.HostBuffer(S * R) as img:
+            dst = torch.from_numpy(img.array).view(S, R)
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                for kv, l in planes[w::workers]:
+                    dst.copy_(pool_b[kv, l])
+                    stream.synchronize()
+                    msg = check(kv, l, img.array.reshape(S, R))
+                    if msg:
+                        errors.append(msg)
+        return errors
+
+    with ThreadPoolExecutor(workers) as ex:
+        return [m for errs in ex.map(work, range(workers)) for m in errs]
+
+
+def _first_bad_row(a: np.ndarray, b: np.ndarray) -> int:
+    rows = np.nonzero(np.any(a != b, axis=1))[0]
+    return int(rows[0]) if rows.size else -1
+
+
+def pool_matches_oracle(pool_t, spans, page_size, layer_range=None, workers=3):
+    """Whole-image parity of a load.  Every (K|V, layer) slab of the GPU pool
+    equals, byte for byte, the oracle's load of `spans` into a slab image that
+    holds the sentinel everywhere (the pool was sentinel-filled before the
+    load); layers outside layer_range equal the untouched sentinel image.
+    spans: (host uint8 array of a token-major chunk, host_tokens, num_tokens,
+    page_idx).  Returns the number of slabs compared."""
+    _, L, S = pool_t.shape[:3]
+    R = pool_t[0, 0, 0].numel() * pool_t.element_size()
+    lo, hi = layer_range or (0, L)
+    live = [(h, ht, nt, np.ascontiguousarray(p, np.int32)) for h, ht, nt, p in spans if nt > 0]
+    expected = {}
+
+    def check(kv, l, image):
+        import threading
+        exp = expected.get(threading.get_ident())
+        if exp is None:
+            exp = expected[threading.get_ident()] = np.empty((S, R), np.uint8)
+        _libc.memset(exp.ctypes.data, SENTINEL & 0xFF, S * R)
+        if lo <= l < hi:
+            for host, ht, nt, pidx in live:
+                a = oracle.host_row_offset(l, kv, ht, 0, R)
+                oracle.load_slab(exp, page_size, host[a:a + nt * R], nt, pidx)
+        if _libc.memcmp(image.ctypes.data, exp.ctypes.data, S * R) != 0:
+            return f"kv {kv} layer {l}: pool slab differs from the oracle (first row {_first_bad_row(image, exp)})"
+        return None
+
+    assert (SENTINEL >> 8) == (SENTINEL & 0xFF)
+    errors = _for_each_slab(pool_t, check, workers)
+    if errors:
+        raise AssertionError(f"{len(errors)} slab(s) differ: " + "; ".join(errors[:4]))
+    return 2 * L
+
+
+def offload_matches_oracle(pool_t, spans, page_size, before_byte, layer_range=None, workers=3):
+    """Whole-chunk parity of an offload.  For every span, every (layer, K|V)
+    slab region of its host chunk equals the oracle's offload of the GPU pool
+    image into a region that held `before_byte` everywhere (the chunk was
+    filled with it before the offload); the pool image itself is checked
+    separately.  spans as for pool_matches_oracle; host arrays are the
+    offload's destinations.  Returns the number of regions compared."""
+    _, L, S = pool_t.shape[:3]
+    R = pool_t[0, 0, 0].numel() * pool_t.element_size()
+    lo, hi = layer_range or (0, L)
+    live = [(h, ht, nt, np.ascontiguousarray(p, np.int32)) for h, ht, nt, p in spans if nt > 0]
+    biggest = max([ht for _, ht, _, _ in live], default=0) * R
+    expected = {}
+
+    def check(kv, l, image):
+        import threading
+        exp = expected.get(threading.get_ident())
+        if exp is None:
+            exp = expected[threading.get_ident()] = np.empty(max(biggest, 1), np.uint8)
+        for i, (host, ht, nt, pidx) in enumerate(live):
+            a = oracle.host_row_offset(l, kv, ht, 0, R)
+            region = exp[:ht * R]
+            _libc.memset(region.ctypes.data, before_byte, ht * R)
+            if lo <= l < hi:
+                oracle.offload_slab(image, page_size, region, nt, pidx)
+            if _libc.memcmp(host[a:a + ht * R].ctypes.data, region.ctypes.data, ht * R) != 0:
+                got = host[a:a + ht * R].reshape(ht, R)
+                return (f"span {i} kv {kv} layer {l}: host chunk differs from the oracle's offload "
+                        f"(first row {_first_bad_row(got, region.reshape(ht, R))})")
+        return None
+
+    errors = _for_each_slab(pool_t, check, workers)
+    if errors:
+        raise AssertionError(f"{len(errors)} region(s) differ: " + "; ".join(errors[:4]))
+    return 2 * L * len(live)
+
+
+def threaded_memset(ptr: int, byte: int, nbytes: int, threads: int = 16, chunk: int = 256 << 20) -> None:
+    """memset of a large host range from several threads."""
+    def one(o):
+        _libc.memset(ptr + o, byte, min(chunk, nbytes - o))
+
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(one, range(0, nbytes, chunk)))

@@ -1,13 +1,17 @@
 """The five evaluation workloads at full size, through the C ABI, in the launch
 configuration bench.py times (library defaults), checked against the CPU
-oracle on sampled rows and by properties that hold at any size:
+oracle element by element:
 
-  * sampled rows: the oracle's slot for (span, layer, kv, token) holds exactly
-    the host row at the oracle's host offset;
-  * untouched slots keep their sentinel and every touched slot changed
-    (plain torch comparisons over the whole pool);
-  * round trip: offloading the loaded context into a fresh chunk reproduces
-    the source chunk byte for byte.
+  * whole pool image: every (K|V, layer) slab of the pool is copied back and
+    compared byte for byte with the oracle's load of the same host chunks into
+    a sentinel-filled slab image (so every moved row is in its slot and every
+    other byte -- untouched slots, partial-page tails, the pages a churn left
+    allocated -- still holds the sentinel);
+  * whole host chunk after an offload: every (layer, K|V) region of the
+    destination chunk equals the oracle's offload of the (checked) pool image
+    into a chunk that held a fill byte before;
+  * round trips and, for the staged path, sampled rows plus sentinel
+    properties.
 
 Inputs are seeded (workloads module): data seed k, placement seed 100 + k,
 churn seed 200 + k for workload k.
@@ -17,7 +21,8 @@ import pytest
 
 import oracle
 import workloads as W
-from _kvtest import SENTINEL, memequal, sampled_rows_match, touched_mask, untouched_rows_hold_sentinel
+from _kvtest import (SENTINEL, memequal, offload_matches_oracle, pool_matches_oracle, sampled_rows_match,
+                     threaded_memset, touched_mask, untouched_rows_hold_sentinel)
 
 pytestmark = pytest.mark.gpu
 
@@ -70,6 +75,9 @@ def test_workload1_tiny_pool_exact(kv):
         pool.close()
 
 
+FILL = 0xA5       # host bytes an offload must overwrite
+
+
 def single_context_workload(kv, k, io_stream, layerwise=False, staged=False):
     import torch
     wl = W.WORKLOADS[k]
@@ -79,6 +87,7 @@ def single_context_workload(kv, k, io_stream, layerwise=False, staged=False):
     nbytes = L * 2 * T * R
     rng = np.random.default_rng(W.placement_seed(k))
     pages = W.random_slots(rng, S, T) if P == 1 else W.random_pages(rng, S // P, -(-T // P))
+    print(f"[workload{k}] layerwise {layerwise} staged {staged}: L={L} S={S} T={T} R={R}", flush=True)
     pool_t = new_pool(L, S, H, D, torch.bfloat16)
     pt = torch.from_numpy(pages).cuda()
     with kv.HostBuffer(nbytes) as hb, kv.HostBuffer(nbytes) as ob:
@@ -96,15 +105,16 @@ def single_context_workload(kv, k, io_stream, layerwise=False, staged=False):
                 compute.wait_event(ev)
                 pool_t[:, l, :1].float().sum()   # a compute-stream consumer of layer l
         else:
-            pool.load(span)
+            pool.load(span, stream=io_stream)
         torch.cuda.synchronize()
         pool.check()
         spans_np = [(hb.array, T, T, pages)]
-        assert sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k) == 4096
-        untouched_rows_hold_sentinel(pool_t, touched_mask(spans_np, P, S), L)
-        pool.offload([(ob.ptr, T, T, pt.data_ptr())])
+        assert pool_matches_oracle(pool_t, spans_np, P, workers=4) == 2 * L
+        threaded_memset(ob.ptr, FILL, nbytes)
+        pool.offload([(ob.ptr, T, T, pt.data_ptr())], stream=io_stream)
         torch.cuda.synchronize()
         pool.check()
+        assert offload_matches_oracle(pool_t, [(ob.array, T, T, pages)], P, FILL, workers=4) == 2 * L
         assert memequal(ob.ptr, hb.ptr, nbytes), "offload round trip differs from the host chunk"
         pool.close()
 
@@ -127,37 +137,77 @@ def test_workload3_staged_layerwise(kv, io_stream):
     single_context_workload(kv, 3, io_stream, layerwise=True, staged=True)
 
 
-@pytest.mark.parametrize("staged", [False, True], ids=["kernel", "staged"])
-def test_workload4_batched_churned(kv, staged):
-    """64 partial-hit contexts of the 8B shape at page size 16 into a churned pool,
-    one batched kvio_load per wave (one wave when host memory allows); staged:
-    both directions through the default 4 GiB of HBM staging each."""
-    import torch
+def batched_setup():
     k = 4
     shp = W.LLAMA8B
+    req = W.batched_requests(k)
+    hit = [int(h) for h in req.hit_tokens]
+    sizes = [shp.num_layers * 2 * h * shp.row_bytes for h in hit]
+    return k, shp, req, hit, sizes, W.batch_waves(sizes, 40 * GiB)
+
+
+N_WAVES = len(batched_setup()[5])
+
+
+@pytest.mark.parametrize("wave", range(N_WAVES))
+def test_workload4_batched_churned_wave(kv, io_stream, wave):
+    """64 partial-hit contexts of the 8B shape at page size 16 into a churned
+    pool, one batched kvio_load per wave, as the benchmark times them.  Each
+    wave is loaded into a sentinel-filled pool and the whole pool image is
+    compared with the oracle's load of that wave's spans (the slots the churn
+    left allocated and every other untouched slot included); then the wave is
+    offloaded with one batched kvio_offload into its own chunks, refilled
+    first, and every chunk is compared with the oracle's offload."""
+    import torch
+    k, shp, req, hit, sizes, waves = batched_setup()
     L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
     R = shp.row_bytes
-    req = W.batched_requests(k)
     S = req.pool_pages * P
-    hit = [int(h) for h in req.hit_tokens]
-    sizes = [L * 2 * h * R for h in hit]
-    # Pinned host memory per process may be capped (64 GiB on some machines), so the
-    # contexts are loaded in waves of at most 40 GiB of host chunks, each wave
-    # one batched kvio_load; the pool holds all of them.
-    budget = 40 * GiB
-    waves, cur, acc = [], [], 0
-    for i, b in enumerate(sizes):
-        if cur and acc + b > budget:
-            waves.append(cur)
-            cur, acc = [], 0
-        cur.append(i)
-        acc += b
-    waves.append(cur)
-    print(f"[workload4] {sum(hit)} tokens, {sum(sizes) / GiB:.1f} GiB, pool {S} slots, "
-          f"{len(waves)} wave(s), mean run length {req.mean_run_length:.2f}, staged {staged}", flush=True)
+    w = waves[wave]
+    nb = sum(sizes[i] for i in w)
+    print(f"[workload4] wave {wave}/{len(waves)}: spans {w[0]}..{w[-1]}, {nb / GiB:.1f} GiB, pool {S} slots, "
+          f"mean run length {req.mean_run_length:.2f}", flush=True)
     torch.cuda.empty_cache()                 # the pool takes most of HBM
     pool_t = new_pool(L, S, H, D, torch.bfloat16)
-    launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED) if staged else None
+    pool = kv.KVPool(pool_t, P)
+    pts = {i: torch.from_numpy(req.page_lists[i]).cuda() for i in w}
+    with kv.HostBuffer(nb) as hb:
+        offs, o = {}, 0
+        for i in w:
+            offs[i] = o
+            W.fill_cuda(hb.ptr + o, sizes[i], W.data_seed(k) * 1000 + i, shp)
+            o += sizes[i]
+        spans = [(hb.ptr + offs[i], hit[i], hit[i], pts[i].data_ptr()) for i in w]
+        pool.load(spans, stream=io_stream)
+        torch.cuda.synchronize()
+        pool.check()
+        spans_np = [(hb.array[offs[i]:offs[i] + sizes[i]], hit[i], hit[i], req.page_lists[i]) for i in w]
+        assert pool_matches_oracle(pool_t, spans_np, P, workers=3) == 2 * L
+        threaded_memset(hb.ptr, FILL, nb)
+        pool.offload(spans, stream=io_stream)
+        torch.cuda.synchronize()
+        pool.check()
+        assert offload_matches_oracle(pool_t, spans_np, P, FILL, workers=3) == 2 * L * len(w)
+    pool.close()
+    del pool_t
+    torch.cuda.empty_cache()
+
+
+def test_workload4_batched_churned_staged(kv):
+    """The batched workload through the staged path (both directions through
+    the default 4 GiB of HBM staging each): every wave loaded into one pool,
+    sampled rows against the oracle, per-span round trips, and the sentinel of
+    every slot no request names (the churn's live pages among them)."""
+    import torch
+    k, shp, req, hit, sizes, waves = batched_setup()
+    L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
+    R = shp.row_bytes
+    S = req.pool_pages * P
+    print(f"[workload4 staged] {sum(hit)} tokens, {sum(sizes) / GiB:.1f} GiB, pool {S} slots, "
+          f"{len(waves)} wave(s)", flush=True)
+    torch.cuda.empty_cache()
+    pool_t = new_pool(L, S, H, D, torch.bfloat16)
+    launch = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
     pool = kv.KVPool(pool_t, P, load_launch=launch, offload_launch=launch)
     pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
     all_spans_np = []
@@ -187,6 +237,8 @@ def test_workload4_batched_churned(kv, staged):
     # churn-resident pages and every slot of no request keep the sentinel
     untouched_rows_hold_sentinel(pool_t, touched_mask(all_spans_np, P, S), L)
     pool.close()
+    del pool_t
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("staged", [False, True], ids=["kernel", "staged_load"])
@@ -230,8 +282,12 @@ def test_workload5_1m_with_concurrent_offload(kv, io_stream, staged):
         print(f"[workload5] {runs} concurrent offload runs during the 1M-token load", flush=True)
         assert memequal(dst_o.ptr, src_o.ptr, nbo), "concurrent offload differs from its source"
         spans_np = [(hb.array, T, T, load_slots), (src_o.array, TO, TO, off_slots)]
-        sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k)
-        untouched_rows_hold_sentinel(pool_t, touched_mask(spans_np, P, S), L)
+        if staged:
+            sampled_rows_match(pool_t, spans_np, P, S, R, L, 4096, seed=k)
+            untouched_rows_hold_sentinel(pool_t, touched_mask(spans_np, P, S), L)
+        else:
+            # two workers: the host chunks here already hold 57.75 GiB of pinned memory
+            assert pool_matches_oracle(pool_t, spans_np, P, workers=2) == 2 * L
         # Round trip in token ranges through a 4 GiB chunk (pinned memory per
         # process may be capped at 64 GiB): offloading tokens
         # [a, b) uses the page table from entry a and a chunk of b - a tokens.

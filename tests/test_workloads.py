@@ -81,3 +81,16 @@ def test_tagged_payload_unique_enough():
     t = W.tagged_payload(2, 64, 2, 8).view(np.uint16)
     assert t.size == 2 * 2 * 64 * 2 * 8
     assert len(np.unique(t)) > 0.9 * min(t.size, 65536) * 0.5
+
+
+def test_batch_waves_split_in_order_within_the_budget():
+    assert W.batch_waves([], 10) == []
+    assert W.batch_waves([4, 4, 4, 4], 8) == [[0, 1], [2, 3]]
+    assert W.batch_waves([9, 1, 1], 8) == [[0], [1, 2]]          # an oversized request goes alone
+    req = W.batched_requests(4)
+    sizes = [32 * 2 * int(h) * 2048 for h in req.hit_tokens]
+    waves = W.batch_waves(sizes, 40 << 30)
+    assert [i for w in waves for i in w] == list(range(64))
+    assert all(sum(sizes[i] for i in w) <= 40 << 30 for w in waves)
+    # fewest waves: no wave could have taken the next wave's first request
+    assert all(sum(sizes[i] for i in a) + sizes[b[0]] > 40 << 30 for a, b in zip(waves, waves[1:]))

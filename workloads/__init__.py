@@ -194,6 +194,26 @@ def batched_requests(k: int = 4, n: int = 64, page_size: int = 16, headroom: flo
     return BatchedRequests(prefix, hit, lists, pool_pages, live_pages, mean_run_length(lists))
 
 
+def batch_waves(sizes: Sequence[int], budget: int = 40 * GiB) -> List[List[int]]:
+    """Split requests, in order, into the fewest consecutive waves whose host
+    chunks total at most `budget` bytes each (a request larger than the budget
+    forms a wave alone).  Pinned host memory per process may be capped (64 GiB
+    on some machines), so the batched workload moves its ~180 GiB in waves,
+    one batched call each."""
+    waves: List[List[int]] = []
+    cur: List[int] = []
+    acc = 0
+    for i, b in enumerate(sizes):
+        if cur and acc + b > budget:
+            waves.append(cur)
+            cur, acc = [], 0
+        cur.append(i)
+        acc += b
+    if cur:
+        waves.append(cur)
+    return waves
+
+
 # ----------------------------------------------------------------------------
 # Payload bytes
 # ----------------------------------------------------------------------------
