@@ -10,7 +10,6 @@
 #include <string.h>
 
 #include <algorithm>
-#include <string>
 #include <vector>
 
 #include "kvio.h"
@@ -19,21 +18,23 @@
 
 namespace {
 
-thread_local std::string g_last_error;
+// Thread-local error text of the last failure (a fixed buffer: recording an
+// error allocates nothing).
+thread_local char g_last_error[1024];
 
 }  // namespace
 
 namespace kvio {
 
 kvio_status fail(kvio_status st, const char *fmt, ...) {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
     va_end(ap);
-    g_last_error = buf;
     return st;
 }
+
+void clear_error() { g_last_error[0] = '\0'; }
 
 kvio_status fail_hip(hipError_t e, const char *what) {
     // The status and the text carry the error; clear the runtime's per-thread
@@ -67,7 +68,11 @@ constexpr int64_t kDefaultStagingBytes = int64_t(4) << 30;
 // amortise (a 2 MiB context: 13 GB/s staged, 52 GB/s through the kernels).
 constexpr int64_t kStagedMinBytes = int64_t(64) << 20;
 
-kvio::Shape resolve(const kvio_launch &l, const kvio::Shape &def) {
+}  // namespace
+
+namespace kvio {
+
+Shape resolve(const kvio_launch &l, const Shape &def) {
     kvio::Shape s;
     s.workgroups = l.workgroups > 0 ? l.workgroups : def.workgroups;
     s.threads = l.threads > 0 ? l.threads : def.threads;
@@ -134,11 +139,64 @@ kvio_status device_view(const void *p, uint64_t bytes, bool want_device_memory, 
     return KVIO_OK;
 }
 
-}  // namespace
+kvio_status check_desc(const kvio_pool_desc *d, const char *fn, PoolGeom *g) {
+    if (d->num_layers < 1 || d->num_kv_heads < 1 || d->head_dim < 1 || d->elem_bytes < 1 ||
+        d->page_size < 1)
+        return fail(KVIO_EINVAL, "%s: sizes must be >= 1", fn);
+    if (d->host_layout != KVIO_HOST_TOKEN_MAJOR && d->host_layout != KVIO_HOST_PAGE_FIRST &&
+        d->host_layout != KVIO_HOST_HEAD_MAJOR)
+        return fail(KVIO_EINVAL, "%s: unknown host layout %d", fn, d->host_layout);
+    if (d->host_layout == KVIO_HOST_HEAD_MAJOR && (int64_t(d->head_dim) * d->elem_bytes) % 16 != 0)
+        return fail(KVIO_EALIGN, "%s: head-major chunks need head_dim * elem_bytes (%lld) to be "
+                    "a multiple of 16", fn, (long long)(int64_t(d->head_dim) * d->elem_bytes));
+    if (d->num_slots < 1 || d->num_slots > INT32_MAX || d->num_slots % d->page_size != 0)
+        return fail(KVIO_EINVAL, "%s: num_slots %lld must be in [1, 2^31) and a multiple "
+                    "of page_size %d", fn, (long long)d->num_slots, d->page_size);
+    const int64_t R = int64_t(d->num_kv_heads) * d->head_dim * d->elem_bytes;
+    if (R % 16 != 0) return fail(KVIO_EALIGN, "%s: row bytes %lld not a multiple of 16", fn, (long long)R);
+    if (R > (int64_t(1) << 26)) return fail(KVIO_EINVAL, "%s: row bytes %lld too large", fn, (long long)R);
+    if (d->k_layers == nullptr || d->v_layers == nullptr) return fail(KVIO_EINVAL, "%s: null layer table", fn);
+    kvio_status st = check_launch(d->load_launch, "load_launch");
+    if (st != KVIO_OK) return st;
+    st = check_launch(d->offload_launch, "offload_launch");
+    if (st != KVIO_OK) return st;
+    g->num_layers = d->num_layers;
+    g->num_heads = d->num_kv_heads;
+    g->host_layout = d->host_layout;
+    g->seg_bytes = int64_t(d->head_dim) * d->elem_bytes;
+    g->page_size = d->page_size;
+    g->num_slots = d->num_slots;
+    g->row_bytes = R;
+    return KVIO_OK;
+}
+
+kvio_status resolve_layers(const kvio_pool_desc *d, const PoolGeom &g, const char *fn, uint8_t **layers) {
+    const uint64_t layer_bytes = uint64_t(g.num_slots) * uint64_t(g.row_bytes);
+    for (int kv = 0; kv < 2; ++kv) {
+        void *const *tab = kv == 0 ? d->k_layers : d->v_layers;
+        for (int l = 0; l < g.num_layers; ++l) {
+            void *ptr = tab[l];
+            if (ptr == nullptr) return fail(KVIO_EINVAL, "%s: %c layer %d is null", fn, kv ? 'V' : 'K', l);
+            if (!aligned16(ptr))
+                return fail(KVIO_EALIGN, "%s: %c layer %d not 16-byte aligned", fn, kv ? 'V' : 'K', l);
+            const uint8_t *dev = nullptr;
+            kvio_status st = device_view(ptr, layer_bytes, true, kv ? "V layer" : "K layer", &dev);
+            if (st != KVIO_OK) return st;
+            layers[size_t(kv) * g.num_layers + l] = const_cast<uint8_t *>(dev);
+        }
+    }
+    return KVIO_OK;
+}
+
+}  // namespace kvio
+
+using kvio::check_launch;
+using kvio::device_view;
+using kvio::resolve;
 
 // Error path shared with kvio_sched.cpp (same thread-local error text).
 kvio_status kvio_sched_fail(kvio_status st, const char *msg) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (st == KVIO_OK) return KVIO_OK;
     return fail(st, "%s", msg);
 }
@@ -201,34 +259,15 @@ const char *kvio_strerror(kvio_status st) {
     return "unknown kvio_status";
 }
 
-const char *kvio_last_error(void) { return g_last_error.c_str(); }
+const char *kvio_last_error(void) { return g_last_error; }
 
 kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (d == nullptr || out == nullptr) return fail(KVIO_EINVAL, "kvio_pool_create: null argument");
-    if (d->num_layers < 1 || d->num_kv_heads < 1 || d->head_dim < 1 || d->elem_bytes < 1 ||
-        d->page_size < 1)
-        return fail(KVIO_EINVAL, "kvio_pool_create: sizes must be >= 1");
-    if (d->host_layout != KVIO_HOST_TOKEN_MAJOR && d->host_layout != KVIO_HOST_PAGE_FIRST &&
-        d->host_layout != KVIO_HOST_HEAD_MAJOR)
-        return fail(KVIO_EINVAL, "kvio_pool_create: unknown host layout %d", d->host_layout);
-    if (d->host_layout == KVIO_HOST_HEAD_MAJOR && (int64_t(d->head_dim) * d->elem_bytes) % 16 != 0)
-        return fail(KVIO_EALIGN, "kvio_pool_create: head-major chunks need head_dim * elem_bytes (%lld) to be "
-                    "a multiple of 16", (long long)(int64_t(d->head_dim) * d->elem_bytes));
-    if (d->num_slots < 1 || d->num_slots > INT32_MAX || d->num_slots % d->page_size != 0)
-        return fail(KVIO_EINVAL, "kvio_pool_create: num_slots %lld must be in [1, 2^31) and a multiple "
-                    "of page_size %d", (long long)d->num_slots, d->page_size);
-    const int64_t R = int64_t(d->num_kv_heads) * d->head_dim * d->elem_bytes;
-    if (R % 16 != 0) return fail(KVIO_EALIGN, "kvio_pool_create: row bytes %lld not a multiple of 16",
-                                 (long long)R);
-    if (R > (int64_t(1) << 26)) return fail(KVIO_EINVAL, "kvio_pool_create: row bytes %lld too large",
-                                            (long long)R);
-    if (d->k_layers == nullptr || d->v_layers == nullptr)
-        return fail(KVIO_EINVAL, "kvio_pool_create: null layer table");
-    kvio_status st = check_launch(d->load_launch, "load_launch");
+    kvio::PoolGeom g;
+    kvio_status st = kvio::check_desc(d, "kvio_pool_create", &g);
     if (st != KVIO_OK) return st;
-    st = check_launch(d->offload_launch, "offload_launch");
-    if (st != KVIO_OK) return st;
+    const int64_t R = g.row_bytes;
     const bool staged[2] = {(d->load_launch.flags & KVIO_LAUNCH_STAGED) != 0,
                             (d->offload_launch.flags & KVIO_LAUNCH_STAGED) != 0};
     const int64_t stage_bytes = d->staging_bytes > 0 ? d->staging_bytes : kDefaultStagingBytes;
@@ -242,40 +281,17 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
 
     kvio_pool *p = new (std::nothrow) kvio_pool();
     if (p == nullptr) return fail(KVIO_ENOMEM, "kvio_pool_create: host allocation failed");
-    p->num_layers = d->num_layers;
-    p->num_heads = d->num_kv_heads;
-    p->host_layout = d->host_layout;
-    p->seg_bytes = int64_t(d->head_dim) * d->elem_bytes;
-    p->page_size = d->page_size;
-    p->num_slots = d->num_slots;
-    p->row_bytes = R;
+    p->g = g;
     p->load_launch = d->load_launch;
     p->offload_launch = d->offload_launch;
     p->layers.resize(2 * size_t(d->num_layers));
     p->d_layers = nullptr;
     p->d_err = nullptr;
     p->slot_bytes = slot_bytes;
-    const uint64_t layer_bytes = uint64_t(d->num_slots) * uint64_t(R);
-    for (int kv = 0; kv < 2; ++kv) {
-        void *const *tab = kv == 0 ? d->k_layers : d->v_layers;
-        for (int l = 0; l < d->num_layers; ++l) {
-            void *ptr = tab[l];
-            if (ptr == nullptr) {
-                delete p;
-                return fail(KVIO_EINVAL, "kvio_pool_create: %c layer %d is null", kv ? 'V' : 'K', l);
-            }
-            if (!aligned16(ptr)) {
-                delete p;
-                return fail(KVIO_EALIGN, "kvio_pool_create: %c layer %d not 16-byte aligned", kv ? 'V' : 'K', l);
-            }
-            const uint8_t *dev = nullptr;
-            st = device_view(ptr, layer_bytes, true, kv ? "V layer" : "K layer", &dev);
-            if (st != KVIO_OK) {
-                delete p;
-                return st;
-            }
-            p->layers[size_t(kv) * d->num_layers + l] = const_cast<uint8_t *>(dev);
-        }
+    st = kvio::resolve_layers(d, g, "kvio_pool_create", p->layers.data());
+    if (st != KVIO_OK) {
+        delete p;
+        return st;
     }
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) {
@@ -301,7 +317,7 @@ kvio_status kvio_pool_create(const kvio_pool_desc *d, kvio_pool_t *out) {
 }
 
 kvio_status kvio_pool_destroy(kvio_pool_t p) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (p == nullptr) return KVIO_OK;
     const hipError_t e = release_pool(p);
     if (e != hipSuccess) return fail_hip(e, "kvio_pool_destroy");
@@ -310,20 +326,17 @@ kvio_status kvio_pool_destroy(kvio_pool_t p) {
 
 }  // extern "C"
 
-namespace {
+namespace kvio {
 
 // Validate the spans and layer range; translate host chunks to device
 // addresses.  Nothing is enqueued here.
-kvio_status validate(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
-                     const char *fn, std::vector<Resolved> *out) {
-    if (p == nullptr) return fail(KVIO_EINVAL, "%s: null pool", fn);
+kvio_status validate_spans(const PoolGeom &g, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                           const char *fn, Resolved *out) {
     if (n < 0) return fail(KVIO_EINVAL, "%s: n_spans %d < 0", fn, n);
     if (n > 0 && spans == nullptr) return fail(KVIO_EINVAL, "%s: null span array", fn);
-    if (l0 < 0 || l1 > p->num_layers || l0 >= l1)
-        return fail(KVIO_EINVAL, "%s: layer range [%d, %d) outside [0, %d)", fn, l0, l1, p->num_layers);
-    out->clear();
-    out->reserve(size_t(n));
-    const int64_t R = p->row_bytes;
+    if (l0 < 0 || l1 > g.num_layers || l0 >= l1)
+        return fail(KVIO_EINVAL, "%s: layer range [%d, %d) outside [0, %d)", fn, l0, l1, g.num_layers);
+    const int64_t R = g.row_bytes;
     for (int32_t i = 0; i < n; ++i) {
         const kvio_span &s = spans[i];
         if (s.num_tokens < 0 || s.host_tokens < 0 || s.num_tokens > s.host_tokens)
@@ -340,18 +353,18 @@ kvio_status validate(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
                 return fail(KVIO_EALIGN, "%s: span %d: page table not 4-byte aligned", fn, i);
             // One past the highest host byte the transfer can touch.
             uint64_t reach;
-            const uint64_t P = uint64_t(p->page_size);
-            if (p->host_layout == KVIO_HOST_PAGE_FIRST) {
-                if (s.host_tokens % p->page_size != 0)
+            const uint64_t P = uint64_t(g.page_size);
+            if (g.host_layout == KVIO_HOST_PAGE_FIRST) {
+                if (s.host_tokens % g.page_size != 0)
                     return fail(KVIO_EINVAL, "%s: span %d: page-first chunks need host_tokens (%lld) to be a "
-                                "multiple of the page size %d", fn, i, (long long)s.host_tokens, p->page_size);
+                                "multiple of the page size %d", fn, i, (long long)s.host_tokens, g.page_size);
                 // whole pages up to the one holding token num_tokens - 1
-                reach = (uint64_t(s.num_tokens) + P - 1) / P * uint64_t(p->num_layers) * 2 * P * uint64_t(R);
-            } else if (p->host_layout == KVIO_HOST_HEAD_MAJOR) {
+                reach = (uint64_t(s.num_tokens) + P - 1) / P * uint64_t(g.num_layers) * 2 * P * uint64_t(R);
+            } else if (g.host_layout == KVIO_HOST_HEAD_MAJOR) {
                 // segment (l1 - 1, V, H - 1, num_tokens - 1)
-                reach = ((uint64_t(l1 - 1) * 2 + 1) * uint64_t(p->num_heads) + uint64_t(p->num_heads) - 1) *
-                            uint64_t(s.host_tokens) * uint64_t(p->seg_bytes) +
-                        uint64_t(s.num_tokens) * uint64_t(p->seg_bytes);
+                reach = ((uint64_t(l1 - 1) * 2 + 1) * uint64_t(g.num_heads) + uint64_t(g.num_heads) - 1) *
+                            uint64_t(s.host_tokens) * uint64_t(g.seg_bytes) +
+                        uint64_t(s.num_tokens) * uint64_t(g.seg_bytes);
             } else {
                 // row (l1 - 1, V, num_tokens - 1)
                 reach = (uint64_t(l1 - 1) * 2 + 1) * uint64_t(s.host_tokens) * uint64_t(R) +
@@ -359,84 +372,73 @@ kvio_status validate(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
             }
             kvio_status st = device_view(s.host, reach, false, "host chunk", &r.host);
             if (st != KVIO_OK) return st;
-            const int64_t pages = (s.num_tokens + p->page_size - 1) / p->page_size;
+            const int64_t pages = (s.num_tokens + g.page_size - 1) / g.page_size;
             const uint8_t *pt = nullptr;
             st = device_view(s.page_idx, uint64_t(pages) * 4u, false, "page table", &pt);
-            if (st != KVIO_OK) return fail(KVIO_EINVAL, "%s: span %d: %s", fn, i, kvio_last_error());
+            if (st != KVIO_OK) {
+                char why[512];
+                snprintf(why, sizeof why, "%s", kvio_last_error());
+                return fail(KVIO_EINVAL, "%s: span %d: %s", fn, i, why);
+            }
             r.page_idx = reinterpret_cast<const int32_t *>(pt);
         }
-        out->push_back(r);
+        out[i] = r;
     }
     return KVIO_OK;
 }
 
-}  // namespace
-
-namespace kvio {
-
 // Fields of a launch that do not depend on its spans.
-void common_args(kvio_pool_t p, const kvio::Shape &shape, int32_t l0, kvio::CopyArgs *a) {
+void common_args(const PoolGeom &g, uint8_t *const *layers, unsigned long long *err, const Shape &shape,
+                 int32_t l0, CopyArgs *a) {
     memset(a, 0, sizeof *a);
-    const int64_t R = p->row_bytes;
-    a->layers = p->d_layers;
-    a->err = p->d_err;
+    const int64_t R = g.row_bytes;
+    a->layers = layers;
+    a->err = err;
     a->row_bytes = R;
-    a->num_pages = p->num_slots / p->page_size;
-    a->num_layers = p->num_layers;
+    a->num_pages = g.num_slots / g.page_size;
+    a->num_layers = g.num_layers;
     a->layer_begin = l0;
-    a->page_size = p->page_size;
-    a->page_shift = ilog2_exact(p->page_size);
+    a->page_size = g.page_size;
+    a->page_shift = ilog2_exact(g.page_size);
     a->vec_per_row = static_cast<int32_t>(R / 16);
     a->vec_shift = ilog2_exact(R / 16);
     a->rows_per_tile = kvio::rows_per_tile(R, shape.tile_kib);
-    a->host_layout = p->host_layout;
-    a->num_heads = p->num_heads;
-    a->seg_vecs = static_cast<int32_t>(p->seg_bytes / 16);
+    a->host_layout = g.host_layout;
+    a->num_heads = g.num_heads;
+    a->seg_vecs = static_cast<int32_t>(g.seg_bytes / 16);
 }
 
-hipError_t launch_capped(const kvio::CopyArgs &a, kvio::Direction dir, kvio::Shape s, hipStream_t stream) {
+void common_args(kvio_pool_t p, const Shape &shape, int32_t l0, CopyArgs *a) {
+    common_args(p->g, p->d_layers, p->d_err, shape, l0, a);
+}
+
+hipError_t launch_capped(const CopyArgs &a, Direction dir, Shape s, hipStream_t stream) {
     const int64_t waves_per_wg = s.threads / 64;
     const int64_t max_wgs = (a.total_tiles + waves_per_wg - 1) / waves_per_wg;
     if (s.workgroups > max_wgs) s.workgroups = static_cast<int>(max_wgs);
-    return kvio::launch_copy(a, dir, s, stream);
+    return launch_copy(a, dir, s, stream);
 }
 
-}  // namespace kvio
-
-namespace {
-
-kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
-                     hipStream_t stream, kvio::Direction dir, const char *fn) {
-    g_last_error.clear();
-    std::vector<Resolved> rs;
-    kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
-    if (st != KVIO_OK) return st;
-    kvio_launch lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
-    if (lc.flags & KVIO_LAUNCH_STAGED) {
-        int64_t bytes = 0;
-        for (const Resolved &r : rs) bytes += r.num_tokens;
-        bytes *= 2 * int64_t(l1 - l0) * p->row_bytes;
-        if (bytes >= std::min(kStagedMinBytes, p->slot_bytes)) {
-            kvio::Shape shape = resolve(lc, kvio::kDefaultStaged);
-            if (p->host_layout == KVIO_HOST_HEAD_MAJOR && p->row_bytes > int64_t(shape.tile_kib) * 1024)
-                shape.head_major_lds = false;
-            return run_staged(p, rs, spans, n, l0, l1, stream, dir, shape, fn);
-        }
-        lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
-    }
-    kvio::Shape shape = resolve(lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);
+Shape kernel_shape(const PoolGeom &g, const kvio_launch &l, const Shape &def) {
+    Shape shape = resolve(l, def);
     // LDS staging of a head-major tile needs the whole tile (>= one row) in the
     // wave's U KiB slice.
-    if (p->host_layout == KVIO_HOST_HEAD_MAJOR && p->row_bytes > int64_t(shape.tile_kib) * 1024)
+    if (g.host_layout == KVIO_HOST_HEAD_MAJOR && g.row_bytes > int64_t(shape.tile_kib) * 1024)
         shape.head_major_lds = false;
+    return shape;
+}
+
+kvio_status launch_spans(const PoolGeom &g, uint8_t *const *layers, unsigned long long *err, const Resolved *rs,
+                         int32_t n, int32_t l0, int32_t l1, Direction dir, const Shape &shape, hipStream_t stream,
+                         const char *fn) {
     for (int32_t first = 0; first < n; first += KVIO_MAX_SPANS_PER_LAUNCH) {
         const int32_t cnt = n - first < KVIO_MAX_SPANS_PER_LAUNCH ? n - first : KVIO_MAX_SPANS_PER_LAUNCH;
-        kvio::CopyArgs a;
-        kvio::common_args(p, shape, l0, &a);
+        CopyArgs a;
+        common_args(g, layers, err, shape, l0, &a);
         a.n_spans = cnt;
         int64_t tiles = 0;
         for (int32_t i = 0; i < cnt; ++i) {
-            const Resolved &r = rs[size_t(first + i)];
+            const Resolved &r = rs[first + i];
             a.tile_prefix[i] = tiles;
             a.spans[i].host = r.host;
             a.spans[i].page_idx = r.page_idx;
@@ -449,23 +451,50 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
         a.plane_tiles = tiles;
         a.total_tiles = tiles * 2 * int64_t(l1 - l0);
         if (a.total_tiles == 0) continue;
-        const hipError_t e = kvio::launch_capped(a, dir, shape, stream);
+        const hipError_t e = launch_capped(a, dir, shape, stream);
         if (e != hipSuccess) return fail_hip(e, fn);
     }
     return KVIO_OK;
 }
 
+}  // namespace kvio
+
+namespace {
+
+kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
+                     hipStream_t stream, kvio::Direction dir, const char *fn) {
+    kvio::clear_error();
+    if (p == nullptr) return fail(KVIO_EINVAL, "%s: null pool", fn);
+    std::vector<Resolved> rs(size_t(n > 0 ? n : 0));
+    kvio_status st = kvio::validate_spans(p->g, spans, n, l0, l1, fn, rs.data());
+    if (st != KVIO_OK) return st;
+    kvio_launch lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
+    if (lc.flags & KVIO_LAUNCH_STAGED) {
+        int64_t bytes = 0;
+        for (const Resolved &r : rs) bytes += r.num_tokens;
+        bytes *= 2 * int64_t(l1 - l0) * p->g.row_bytes;
+        if (bytes >= std::min(kStagedMinBytes, p->slot_bytes))
+            return run_staged(p, rs, spans, n, l0, l1, stream, dir,
+                              kvio::kernel_shape(p->g, lc, kvio::kDefaultStaged), fn);
+        lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
+    }
+    const kvio::Shape shape =
+        kvio::kernel_shape(p->g, lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);
+    return kvio::launch_spans(p->g, p->d_layers, p->d_err, rs.data(), n, l0, l1, dir, shape, stream, fn);
+}
+
 kvio_status run_naive(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
                       hipStream_t stream, kvio::Direction dir, const char *fn) {
-    g_last_error.clear();
-    std::vector<Resolved> rs;
-    kvio_status st = validate(p, spans, n, l0, l1, fn, &rs);
+    kvio::clear_error();
+    if (p == nullptr) return fail(KVIO_EINVAL, "%s: null pool", fn);
+    std::vector<Resolved> rs(size_t(n > 0 ? n : 0));
+    kvio_status st = kvio::validate_spans(p->g, spans, n, l0, l1, fn, rs.data());
     if (st != KVIO_OK) return st;
-    if (p->host_layout == KVIO_HOST_HEAD_MAJOR)
+    if (p->g.host_layout == KVIO_HOST_HEAD_MAJOR)
         return fail(KVIO_EINVAL, "%s: the per-page copy baseline takes token-major or page-first chunks", fn);
-    const int64_t R = p->row_bytes;
-    const int64_t P = p->page_size;
-    const int64_t num_pages = p->num_slots / P;
+    const int64_t R = p->g.row_bytes;
+    const int64_t P = p->g.page_size;
+    const int64_t num_pages = p->g.num_slots / P;
     std::vector<int32_t> table;
     for (int32_t i = 0; i < n; ++i) {
         const kvio_span &s = spans[i];
@@ -481,13 +510,13 @@ kvio_status run_naive(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t 
         uint8_t *host = static_cast<uint8_t *>(s.host);
         for (int32_t l = l0; l < l1; ++l) {
             for (int kv = 0; kv < 2; ++kv) {
-                uint8_t *pool = p->layers[size_t(kv) * p->num_layers + l];
+                uint8_t *pool = p->layers[size_t(kv) * p->g.num_layers + l];
                 uint8_t *hrow0 = host + ((int64_t(l) * 2 + kv) * s.host_tokens) * R;
                 for (int64_t j = 0; j < pages; ++j) {
                     const int64_t rows = (j + 1) * P <= s.num_tokens ? P : s.num_tokens - j * P;
                     uint8_t *prow = pool + int64_t(table[size_t(j)]) * P * R;
-                    uint8_t *hrow = p->host_layout == KVIO_HOST_PAGE_FIRST
-                        ? host + ((j * p->num_layers + l) * 2 + kv) * P * R
+                    uint8_t *hrow = p->g.host_layout == KVIO_HOST_PAGE_FIRST
+                        ? host + ((j * p->g.num_layers + l) * 2 + kv) * P * R
                         : hrow0 + j * P * R;
                     hipError_t e2 = dir == kvio::kLoad
                         ? hipMemcpyAsync(prow, hrow, size_t(rows * R), hipMemcpyHostToDevice, stream)
@@ -526,7 +555,7 @@ kvio_status kvio_load_layer(kvio_pool_t p, const kvio_span *spans, int32_t n, in
 }
 
 kvio_status kvio_check(kvio_pool_t p) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (p == nullptr) return fail(KVIO_EINVAL, "kvio_check: null pool");
     hipError_t e = hipDeviceSynchronize();
     if (e != hipSuccess) return fail_hip(e, "kvio_check: hipDeviceSynchronize");
@@ -539,7 +568,7 @@ kvio_status kvio_check(kvio_pool_t p) {
     const unsigned long long span = (rec >> kvio::kErrSpanShift) - 1;
     const unsigned long long page = rec & ((1ull << kvio::kErrSpanShift) - 1);
     return fail(KVIO_ERANGE, "kvio_check: span %llu, context page %llu: pool page index outside [0, %lld); "
-                "those rows were skipped", span, page, (long long)(p->num_slots / p->page_size));
+                "those rows were skipped", span, page, (long long)(p->g.num_slots / p->g.page_size));
 }
 
 kvio_status kvio_naive_load(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l0, int32_t l1,
@@ -553,7 +582,7 @@ kvio_status kvio_naive_offload(kvio_pool_t p, const kvio_span *spans, int32_t n,
 }
 
 kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (bytes == 0) return KVIO_OK;
     if (dst == nullptr || src == nullptr) return fail(KVIO_EINVAL, "kvio_memcpy: null pointer");
     hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, stream);
@@ -562,7 +591,7 @@ kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t st
 }
 
 kvio_status kvio_stream_create(const uint32_t *cu_mask, uint32_t mask_words, hipStream_t *out) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (out == nullptr) return fail(KVIO_EINVAL, "kvio_stream_create: null out");
     hipStream_t s = nullptr;
     hipError_t e;
@@ -581,7 +610,7 @@ kvio_status kvio_stream_create(const uint32_t *cu_mask, uint32_t mask_words, hip
 }
 
 kvio_status kvio_stream_destroy(hipStream_t stream) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (stream == nullptr) return fail(KVIO_EINVAL, "kvio_stream_destroy: null stream");
     hipError_t e = hipStreamDestroy(stream);
     if (e != hipSuccess) return fail_hip(e, "kvio_stream_destroy");
@@ -589,7 +618,7 @@ kvio_status kvio_stream_destroy(hipStream_t stream) {
 }
 
 kvio_status kvio_host_alloc(size_t bytes, uint32_t flags, void **out) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (out == nullptr || bytes == 0) return fail(KVIO_EINVAL, "kvio_host_alloc: null out or zero size");
     if ((flags & ~uint32_t(KVIO_HOST_NONCOHERENT)) != 0)
         return fail(KVIO_EINVAL, "kvio_host_alloc: unknown flags 0x%x", flags);
@@ -608,7 +637,7 @@ kvio_status kvio_host_alloc(size_t bytes, uint32_t flags, void **out) {
 }
 
 kvio_status kvio_host_free(void *ptr) {
-    g_last_error.clear();
+    kvio::clear_error();
     if (ptr == nullptr) return KVIO_OK;
     hipError_t e = hipHostFree(ptr);
     if (e != hipSuccess) return fail_hip(e, "kvio_host_free");

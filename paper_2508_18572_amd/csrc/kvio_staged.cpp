@@ -37,7 +37,7 @@ namespace kvio {
 kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvio_span *spans, int32_t n,
                        int32_t l0, int32_t l1, hipStream_t stream, kvio::Direction dir, const kvio::Shape &shape,
                        const char *fn) {
-    const int64_t R = p->row_bytes, P = p->page_size, cap = p->slot_bytes;
+    const int64_t R = p->g.row_bytes, P = p->g.page_size, cap = p->slot_bytes;
     if (p->stage[dir] == nullptr) return fail(KVIO_EINVAL, "%s: the pool has no staging buffer for this direction", fn);
     hipStream_t ks = p->side_stream[dir];
     struct Unit { int32_t span; int64_t t0, n, off; };
@@ -62,8 +62,8 @@ kvio_status run_staged(kvio_pool_t p, const std::vector<Resolved> &rs, const kvi
             return one(host + int64_t(lb) * 2 * ht * R, slot + u.off, int64_t(g) * 2 * u.n * R);
         // Token runs of one plane: contiguous rows (token-major), or one run
         // of head segments per head (head-major: [H][host_tokens][De]).
-        const bool hm = p->host_layout == KVIO_HOST_HEAD_MAJOR;
-        const int64_t runs = hm ? p->num_heads : 1, run = hm ? p->seg_bytes : R;
+        const bool hm = p->g.host_layout == KVIO_HOST_HEAD_MAJOR;
+        const int64_t runs = hm ? p->g.num_heads : 1, run = hm ? p->g.seg_bytes : R;
         for (int32_t l = lb; l < lb + g; ++l)
             for (int kv = 0; kv < 2; ++kv)
                 for (int64_t h = 0; h < runs; ++h) {
