@@ -1,17 +1,23 @@
 """Benchmark of the paged-KV host<->HBM transfer path on one MI355X.
 
-Default workload: Llama-3.1-8B KV (32 layers, K and V, 8 KV heads x 128 dims,
-bf16, 128 KiB per token), a pool of 500,000 token slots at page size 1, and
-one 32K-token cached prefix placed in slots drawn uniformly at random (worst
-case fragmentation).  One step = one pass of the hot path over that context:
-kvio_load of all layers (host chunk -> scattered pool slots) followed by
-kvio_offload of all layers (pool slots -> a second host chunk), each one
-kernel launch on the same stream.
+Default run (the headline): the batched workload 4 -- 64 cached contexts of
+the Llama-3.1-8B KV shape (32 layers, K and V, 8 KV heads x 128 dims, bf16,
+128 KiB per token) with prefixes log-uniform in [2K, 128K) tokens and 50-100%
+hits, 1.48 M tokens = 180 GiB per direction, in a pool of 1.7 M slots at page
+size 16 fragmented by a seeded 10,000-op allocate/free churn.  Pinned host
+memory per process may be capped (64 GiB on some machines), so the contexts
+move in 6 waves of at most 40 GiB through one host buffer.  Set-up (untimed)
+fills every wave's chunk and loads it, so the pool holds all contexts.  One
+step = for every wave, one batched kvio_offload (pool -> host) and one batched
+kvio_load (host -> pool) of the wave's contexts.  Workloads 1, 2, 3 and 5 are
+measured afterwards (--other-reps repetitions each) and summarised in the same
+line under "other_workloads".
 
 Reported (one JSON line):
   value       effective GB/s (1e9 B/s) of the whole step: load + offload
-              payload bytes / mean step time; inputs are resident (host chunk
-              pinned, pool in HBM) before the timed region.
+              payload bytes / mean step time (HIP events on the transfer
+              stream); inputs are resident (host chunks pinned, pool in HBM)
+              before the timed region.
   load/offload per-direction GB/s and tokens/s, each against the measured
               contiguous hipMemcpyAsync peak of the same direction, measured in the
               same run.
@@ -21,14 +27,15 @@ Reported (one JSON line):
               with the ratio to the measured contiguous memcpy peak beside
               it; HBM side too; traffic from the committed rocprofv3 counters
               while the kernel sources match them.
-  naive       the per-page hipMemcpyAsync baseline on a prefix of the calls.
-  cpu_baseline the CPU oracle, single thread, on the same context.
+  cpu_baseline the CPU oracle on the contexts of one wave, one core and all
+              cores.
 
-Other workloads: --config 1 (tiny pool, P = 16), --config 3 (70B KV, P = 16,
-layer-wise load on a side stream against a per-layer bf16 GEMM), --config 4
-(64 batched partial hits in a churned pool), --config 5 (1M-token load with
-concurrent offloads); --staged (copy engine + HBM scatter), --interference,
---page-sweep, --row-sweep, --schedule, --disk.
+Other workloads alone: --config 1 (tiny pool, P = 16), --config 2 (Llama-3.1-8B
+KV, P = 1, one 32K-token context), --config 3 (70B KV, P = 16, layer-wise load
+on a side stream against a per-layer bf16 GEMM), --config 4 (the headline
+without the others), --config 5 (1M-token load with concurrent offloads);
+--staged (copy engine + HBM scatter), --interference, --page-sweep,
+--row-sweep, --schedule, --disk.
 """
 from __future__ import annotations
 
@@ -56,7 +63,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=0, choices=[0, 1, 2, 3, 4, 5],
+                    help="0 (default): the batched workload 4 is the headline and workloads 1, 2, 3 and 5 "
+                         "are measured after it, in the same JSON line; 1-5: that workload alone")
+    ap.add_argument("--other-reps", type=int, default=5,
+                    help="timed repetitions of each other workload in the default run (reported as reps)")
+    ap.add_argument("--no-other-workloads", action="store_true")
     ap.add_argument("--workgroups", type=int, default=0)
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--tile-kib", type=int, default=0)
@@ -103,14 +115,20 @@ def parse():
     return ap.parse_args()
 
 
+COUNTER_FILES = {2: "kvio_copy_kernel__llama8b_p1_32k.counters.txt",
+                 4: "kvio_copy_kernel__llama8b_p16_batched.counters.txt"}
+
+
 def measured_traffic(config, default_launch):
     """HBM/link bytes per load launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernels: the kernel source and
-    the header that holds the kernel arguments and default launch shapes
-    (else None)."""
+    summary of a workload, if it was taken on the current kernels: the kernel
+    source and the header that holds the kernel arguments and default launch
+    shapes (else None).  A summary over several launches (load_launches) gives
+    their mean."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "kvio_copy_kernel__llama8b_p1_32k.counters.txt")
-    if config != 2 or not default_launch or not os.path.exists(path):
+    name = COUNTER_FILES.get(config)
+    path = os.path.join(ROOT, "profiles", name) if name else None
+    if not path or not default_launch or not os.path.exists(path):
         return None
     kv = {}
     for line in open(path):
@@ -122,8 +140,9 @@ def measured_traffic(config, default_launch):
                    for f in ("kvio_kernels.hip", "kvio_internal.h"))
     if cur != kv.get("kernel_sources_sha256"):
         return None
-    fetch = float(kv["load_fetch_kib"]) * float(kv["fetch_scale"]) * 1024
-    write = float(kv["load_write_kib"]) * float(kv["write_scale"]) * 1024
+    launches = float(kv.get("load_launches", 1))
+    fetch = float(kv["load_fetch_kib"]) * float(kv["fetch_scale"]) * 1024 / launches
+    write = float(kv["load_write_kib"]) * float(kv["write_scale"]) * 1024 / launches
     return {"bytes": round(fetch + write), "fetch_bytes": round(fetch), "write_bytes": round(write),
             "source": os.path.relpath(path, ROOT)}
 
@@ -563,7 +582,7 @@ def run_layerwise(args, torch, kv, W):
         loads_alone()
         gemms_alone()
         both()
-    reps = max(1, min(args.steps, 5))
+    reps = max(1, args.steps)
     tl = statistics.median(loads_alone() for _ in range(reps))
     tg = statistics.median(gemms_alone() for _ in range(reps))
     runs = [both() for _ in range(reps)]
@@ -594,17 +613,86 @@ def run_layerwise(args, torch, kv, W):
         "host_link_peak": peak_report(peak),
         "roofline": roofline("kvio_copy_kernel<load> (per layer)", load_gbps, peak["h2d"] if peak else None,
                              algorithmic_bytes_per_launch=per_layer),
+        "reps": reps,
     })
     pool.close()
+    del pool_t
     host.free()
-    print(json.dumps(res), flush=True)
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline_batched(slab_rows, row_bytes, chunk, spans, page_size, L, seconds, threads):
+    """The CPU oracle, unchanged, on the spans of one wave of the batched
+    workload: load then offload of every span, one (layer, K|V) slab at a
+    time, into one host image of a pool slab (S rows), plane after plane until
+    `seconds` have passed.  With threads > 1 the spans are cut into pieces of
+    whole pages (at most 8192 tokens) that the threads share out; pieces write
+    disjoint rows of the one slab image and offload into buffers of their
+    own.  spans: (byte offset of the chunk in `chunk`, host_tokens,
+    num_tokens, page_idx).  Returns (bytes moved, seconds, planes done)."""
+    import threading
+
+    import oracle
+    R = row_bytes
+    piece = 8192 - 8192 % page_size if page_size <= 8192 else page_size
+    items = []
+    for off, ht, nt, pages in spans:
+        for a in range(0, nt, piece):
+            items.append((off, ht, a, min(piece, nt - a), pages[a // page_size:]))
+    slab = np.zeros((slab_rows, R), np.uint8)
+    slab.fill(1)                     # touch every page before the clock starts
+    planes = [(l, kvi) for l in range(L) for kvi in range(2)]
+    done = [0] * threads
+    moved = [0] * threads
+    stop = threading.Event()
+
+    def work(w):
+        mine = items[w::threads]
+        out = np.ones(max([n for _, _, _, n, _ in mine], default=1) * R, np.uint8)
+        i = 0
+        while not stop.is_set():
+            l, kvi = planes[i % len(planes)]
+            for off, ht, a, n, pages in mine:
+                base = off + ((l * 2 + kvi) * ht + a) * R
+                oracle.load_slab(slab, page_size, chunk[base:base + n * R], n, pages)
+                oracle.offload_slab(slab, page_size, out, n, pages)
+                moved[w] += 2 * n * R
+            done[w] += 1
+            i += 1
+            if threads == 1 and time.perf_counter() - t0 >= seconds:
+                break
+
+    if threads == 1:
+        t0 = time.perf_counter()
+        work(0)
+    else:
+        workers = [threading.Thread(target=work, args=(w,)) for w in range(threads)]
+        t0 = time.perf_counter()
+        for t in workers:
+            t.start()
+        time.sleep(seconds)
+        stop.set()
+        for t in workers:
+            t.join()
+    el = time.perf_counter() - t0
+    return sum(moved), el, min(done)
 
 
 def run_batched(args, torch, kv, W):
-    """64 partial-hit contexts of the 8B shape at page size 16 into a pool
-    fragmented by a seeded allocate/free churn; one batched kvio_load per wave
-    of contexts (pinned host memory per process may be capped, at 64 GiB on
-    some machines, so the host chunks are staged in waves of <= 40 GiB)."""
+    """The batched workload: 64 partial-hit contexts of the Llama-3.1-8B KV
+    shape at page size 16, placed in a pool fragmented by a seeded 10,000-op
+    allocate/free churn.  Pinned host memory per process may be capped (64 GiB
+    on some machines), so the ~180 GiB of host chunks move in waves of at most
+    40 GiB through one host buffer, one batched call per wave and direction.
+
+    Set-up (untimed): every wave's chunk is filled with its seeded payload and
+    loaded, so the pool holds all 64 contexts.  One step = for every wave, a
+    batched kvio_offload of the wave's contexts from the pool into the host
+    buffer, then a batched kvio_load of them back into their pages: every
+    context crosses the host link once in each direction, and the data a load
+    moves is the data its offload wrote.  Every step is timed with HIP events
+    on the transfer stream, each launch with its own pair."""
     k = 4
     shp = W.LLAMA8B
     L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
@@ -613,72 +701,130 @@ def run_batched(args, torch, kv, W):
     S = req.pool_pages * P
     hit = [int(h) for h in req.hit_tokens]
     sizes = [L * 2 * h * R for h in hit]
-    budget = 40 << 30
-    waves, cur, acc = [], [], 0
-    for i, b in enumerate(sizes):
-        if cur and acc + b > budget:
-            waves.append(cur)
-            cur, acc = [], 0
-        cur.append(i)
-        acc += b
-    waves.append(cur)
+    waves = W.batch_waves(sizes, 40 << 30)
     total = sum(sizes)
-    log(f"batched partial hits: {sum(hit)} tokens, {total / 2**30:.1f} GiB, pool {S} slots, {len(waves)} waves, "
-        f"mean page-run length {req.mean_run_length:.2f}")
+    wave_bytes = [sum(sizes[i] for i in w) for w in waves]
+    log(f"batched partial hits: {sum(hit)} tokens, {total / 2**30:.1f} GiB per direction, pool {S} slots, "
+        f"{len(waves)} waves, mean page-run length {req.mean_run_length:.2f}")
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    torch.cuda.empty_cache()
     pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
     lc = launch_from(args, kv)
     pool = kv.KVPool(pool_t, P, load_launch=lc, offload_launch=lc, staging_bytes=args.staging_mib << 20)
     pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
-    host = kv.HostBuffer(max(sum(sizes[i] for i in w) for w in waves))
-    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    host = kv.HostBuffer(max(wave_bytes))
     stream = io_stream(torch, kv)
-    reps = max(1, min(args.steps, 3))
-    load_ms, off_ms = [], []
+    wave_spans, offs_of = [], []
     for w in waves:
         offs, o = {}, 0
         for i in w:
             offs[i] = o
-            W.fill_cuda(host.ptr + o, sizes[i], W.data_seed(k) * 1000 + i, shp)
             o += sizes[i]
-        spans = [(host.ptr + offs[i], hit[i], hit[i], pts[i].data_ptr()) for i in w]
-        pool.load(spans, stream=stream)                    # warm-up
+        offs_of.append(offs)
+        wave_spans.append([(host.ptr + offs[i], hit[i], hit[i], pts[i].data_ptr()) for i in w])
+    t0 = time.perf_counter()
+    for j, (w, spans) in enumerate(zip(waves, wave_spans)):
+        for i in w:
+            W.fill_cuda(host.ptr + offs_of[j][i], sizes[i], W.data_seed(k) * 1000 + i, shp)
+        pool.load(spans, stream=stream)
         torch.cuda.synchronize()
-        tl, to = Timer(torch, stream), Timer(torch, stream)
-        for _ in range(reps):
-            e = tl.start()
-            pool.load(spans, stream=stream)
-            tl.stop(e)
-        for _ in range(reps):                                # offload back into the same chunks
+    pool.check()
+    log(f"set-up: {len(waves)} waves filled and loaded in {time.perf_counter() - t0:.1f} s")
+
+    def step(tl, to):
+        for spans in wave_spans:
             e = to.start()
             pool.offload(spans, stream=stream)
             to.stop(e)
-        torch.cuda.synchronize()
-        load_ms.append(statistics.median(tl.ms()))
-        off_ms.append(statistics.median(to.ms()))
+            e = tl.start()
+            pool.load(spans, stream=stream)
+            tl.stop(e)
+
+    for _ in range(args.warmup):
+        step(Timer(torch, stream), Timer(torch, stream))
+    torch.cuda.synchronize()
+    tl, to, tstep = Timer(torch, stream), Timer(torch, stream), Timer(torch, stream)
+    w0 = time.perf_counter()
+    for _ in range(args.steps):
+        e = tstep.start()
+        step(tl, to)
+        tstep.stop(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
     pool.check()
-    tload, toff = sum(load_ms), sum(off_ms)
-    load_gbps, off_gbps = total / (tload * 1e-3) / GB, total / (toff * 1e-3) / GB
-    log(f"batched load {load_gbps:.2f} GB/s, offload {off_gbps:.2f} GB/s over {len(waves)} waves")
-    res = base_result(args, load_gbps, tload, "batched partial hits of the Llama-3.1-8B KV shape, "
-                      "page size 16, churned pool",
+    load_ms, off_ms, step_ms = tl.ms(), to.ms(), tstep.ms()
+    n_w = len(waves)
+    # per-step totals (every step moves every wave once in each direction)
+    t_load = sum(load_ms) / args.steps
+    t_off = sum(off_ms) / args.steps
+    t_step = statistics.mean(step_ms)
+    load_gbps, off_gbps = total / (t_load * 1e-3) / GB, total / (t_off * 1e-3) / GB
+    value = 2 * total / (t_step * 1e-3) / GB
+    wave_load_ms = [statistics.mean(load_ms[j::n_w]) for j in range(n_w)]
+    log(f"step {t_step:.1f} ms ({value:.2f} GB/s both directions), wall {wall / args.steps * 1e3:.1f} ms/step; "
+        f"load {load_gbps:.2f} GB/s, offload {off_gbps:.2f} GB/s over {n_w} waves")
+
+    # the data survived every round trip: the last wave's first context against its seed
+    i0 = waves[-1][0]
+    with kv.HostBuffer(sizes[i0]) as ref:
+        W.fill_cuda(ref.ptr, sizes[i0], W.data_seed(k) * 1000 + i0, shp)
+        ok = memequal_ptr(host.ptr + offs_of[-1][i0], ref.ptr, sizes[i0])
+    assert ok, "the batched round trips changed a context's bytes"
+
+    cpu = cpu_all = None
+    if not args.no_cpu_baseline:
+        # the first (largest) wave's contexts, brought back into the host buffer untimed
+        pool.offload(wave_spans[0], stream=stream)
+        torch.cuda.synchronize()
+        first = [(offs_of[0][i], hit[i], hit[i], req.page_lists[i]) for i in waves[0]]
+        desc = (f"the {len(first)} contexts of the first wave ({wave_bytes[0] / 2**30:.1f} GiB per direction), "
+                f"load + offload one (layer, K|V) slab at a time through a {S}-row host slab image")
+        nb, el, planes = cpu_baseline_batched(S, R, host.array, first, P, L, args.cpu_seconds, 1)
+        cpu = {"value": round(nb / el / GB, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"{desc}: {planes} plane(s) in {el:.1f} s on {cpu_model()} "
+                         f"({len(os.sched_getaffinity(0))} cores available, 1 used)"}
+        nthreads = min(len(os.sched_getaffinity(0)), 16)
+        nb, el, planes = cpu_baseline_batched(S, R, host.array, first, P, L, args.cpu_seconds, nthreads)
+        cpu_all = {"value": round(nb / el / GB, 3), "unit": "GB/s", "cores": nthreads, "kind": "oracle",
+                   "sample": f"{desc}, pieces of <= 8192 tokens shared by {nthreads} threads: "
+                             f"{planes}+ plane(s) in {el:.1f} s on {cpu_model()}"}
+        log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core, {cpu_all['value']:.2f} GB/s on {nthreads} threads")
+
+    default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.staged)
+    traffic = measured_traffic(4, default_launch)
+    res = base_result(args, value, t_step, "batched partial hits (workload 4): 64 Llama-3.1-8B KV contexts, "
+                      "page size 16, prefixes log-uniform in [2K, 128K) tokens with 50-100% hits, in a pool "
+                      "fragmented by a 10,000-op allocate/free churn",
                       {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "requests": len(hit),
-                       "tokens": sum(hit), "payload_bytes": total, "waves": len(waves),
-                       "mean_page_run_length": round(req.mean_run_length, 3),
-                       "step": "one batched kvio_load per wave, all waves"})
+                       "tokens": sum(hit), "payload_bytes_per_direction": total, "waves": n_w,
+                       "wave_payload_bytes": wave_bytes, "mean_page_run_length": round(req.mean_run_length, 3),
+                       "step": "for each wave: batched kvio_offload (pool -> host) then batched kvio_load "
+                               "(host -> pool) of the wave's contexts"})
     res.update({
-        "tokens_per_s": round(sum(hit) / (tload * 1e-3), 1),
-        "load": {"gbps": round(load_gbps, 3), "ms": round(tload, 3),
+        "tokens_per_s": round(2 * sum(hit) / (t_step * 1e-3), 1),
+        "load": {"gbps": round(load_gbps, 3), "ms_per_step": round(t_load, 3),
+                 "tokens_per_s": round(sum(hit) / (t_load * 1e-3), 1),
                  "frac_of_h2d_peak": round(load_gbps / peak["h2d"], 4) if peak else None},
-        "offload": {"gbps": round(off_gbps, 3), "ms": round(toff, 3),
+        "offload": {"gbps": round(off_gbps, 3), "ms_per_step": round(t_off, 3),
+                    "tokens_per_s": round(sum(hit) / (t_off * 1e-3), 1),
                     "frac_of_d2h_peak": round(off_gbps / peak["d2h"], 4) if peak else None},
-        "wave_load_ms": [round(x, 3) for x in load_ms],
+        "frac_of_host_link_peak": round((total / (peak["h2d"] * GB) + total / (peak["d2h"] * GB)) * 1e3 / t_step, 4)
+        if peak else None,
+        "wave_load_ms": [round(x, 3) for x in wave_load_ms],
         "host_link_peak": peak_report(peak),
-        "roofline": roofline("kvio_copy_kernel<load> (batched spans)", load_gbps, peak["h2d"] if peak else None,
-                             algorithmic_bytes_per_launch=round(total / len(waves))),
+        "roofline": roofline("kvio_copy_kernel<load> (batched spans, one launch per wave)", load_gbps,
+                             peak["h2d"] if peak else None, traffic=traffic,
+                             algorithmic_bytes_per_launch=round(total / n_w),
+                             algorithmic_traffic_per_launch=round(2 * total / n_w),
+                             launches_per_step=n_w),
+        "cpu_baseline": cpu,
+        "cpu_baseline_all_cores": cpu_all,
     })
     pool.close()
+    del pool_t
     host.free()
-    print(json.dumps(res), flush=True)
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_bidirectional(args, torch, kv, W):
@@ -730,7 +876,7 @@ def run_bidirectional(args, torch, kv, W):
     t_off_alone = statistics.median(toa.ms())
     n_off = int(t_load_alone / t_off_alone * 1.5) + 4
     # concurrent
-    reps = max(1, min(args.steps, 3))
+    reps = max(1, args.steps)
     rows = []
     for _ in range(reps):
         torch.cuda.synchronize()
@@ -781,12 +927,15 @@ def run_bidirectional(args, torch, kv, W):
         "roofline": roofline("kvio_copy_kernel<load> || <offload>", bidir, peak["bidir"] if peak else None,
                              directions=2, algorithmic_bytes_per_launch=nb),
     })
+    res["reps"] = reps
     pool.close()
     pool_bg.close()
+    del pool_t
     host.free()
     src_o.free()
     dst_o.free()
-    print(json.dumps(res), flush=True)
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_interference(args, torch, kv, W):
@@ -999,6 +1148,15 @@ def run_row_sweep(args, torch, kv, W):
     res["host_link_peak"] = peak_report(peak)
     res["sweep"] = rows
     print(json.dumps(res), flush=True)
+
+
+def memequal_ptr(a_ptr, b_ptr, n):
+    """Bytes [a_ptr, a_ptr + n) == [b_ptr, b_ptr + n) of host memory (libc memcmp)."""
+    import ctypes
+    libc = ctypes.CDLL("libc.so.6")
+    libc.memcmp.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]
+    libc.memcmp.restype = ctypes.c_int
+    return libc.memcmp(a_ptr, b_ptr, n) == 0
 
 
 def memequal_np(a, b, n):
@@ -1388,6 +1546,42 @@ def run_disk(args, torch, kv, W):
 EXTRA_MODES = {3: run_layerwise, 4: run_batched, 5: run_bidirectional}
 
 
+def run_other_workloads(args, torch, kv, W):
+    """Workloads 1, 2, 3 and 5 after the headline, each with --other-reps
+    timed repetitions (2 warm-ups), summarised for the same JSON line."""
+    sub = argparse.Namespace(**vars(args))
+    sub.steps, sub.warmup, sub.no_cpu_baseline = max(1, args.other_reps), min(args.warmup, 2), True
+    out = {}
+    r = run_single(sub, torch, kv, W, 1)
+    st = r.get("steady_state", {})
+    out["workload_1"] = {
+        "workload": r["config"]["workload"], "reps": sub.steps,
+        "steady_state_load_gbps": st.get("load_gbps"), "frac_of_h2d_peak": st.get("load_frac_of_h2d_peak"),
+        "steady_state_loads": st.get("reps"), "single_shot_us": st.get("single_shot_us"),
+        "batched4_load_gbps": st.get("batched4_load_gbps"), "two_streams_load_gbps": st.get("two_streams_load_gbps")}
+    r = run_single(sub, torch, kv, W, 2)
+    out["workload_2"] = {
+        "workload": r["config"]["workload"], "reps": sub.steps, "step_gbps": r["value"],
+        "ms_per_step": r["ms_per_step"], "load_gbps": r["load"]["gbps"],
+        "load_frac_of_h2d_peak": r["load"]["frac_of_h2d_peak"], "offload_gbps": r["offload"]["gbps"],
+        "offload_frac_of_d2h_peak": r["offload"]["frac_of_d2h_peak"], "tokens_per_s": r["tokens_per_s"],
+        "naive_per_page_memcpy_gbps": round(r["naive"]["gbps"], 3) if r.get("naive") else None}
+    r = run_layerwise(sub, torch, kv, W)
+    lw = r["layerwise"]
+    out["workload_3"] = {
+        "workload": r["config"]["workload"], "reps": r["reps"], "load_gbps_alone": lw["load_gbps_alone"],
+        "load_gbps_beside_gemms": lw["load_gbps_corun"], "load_frac_of_h2d_peak": r["load"]["frac_of_h2d_peak"],
+        "overlap_efficiency": lw["overlap_efficiency"], "gemm_slowdown": lw["gemm_slowdown"],
+        "t_both_ms": lw["t_both_ms"]}
+    r = run_bidirectional(sub, torch, kv, W)
+    out["workload_5"] = {
+        "workload": r["config"]["workload"], "reps": r["reps"], "bidirectional_gbps": r["bidirectional_gbps"],
+        "frac_of_bidir_peak": r["frac_of_bidir_peak"], "load_gbps_concurrent": r["load"]["gbps_concurrent"],
+        "offload_gbps_concurrent": r["offload"]["gbps_concurrent"], "load_gbps_alone": r["load"]["gbps_alone"],
+        "offload_gbps_alone": r["offload"]["gbps_alone"]}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -1427,10 +1621,15 @@ def main():
             run_row_sweep(args, torch, kv, W)
         elif args.schedule:
             run_schedule(args, torch, kv, W)
+        elif k == 0:
+            res = run_batched(args, torch, kv, W)
+            if not args.no_other_workloads:
+                res["other_workloads"] = run_other_workloads(args, torch, kv, W)
+            print(json.dumps(res), flush=True)
         elif k in EXTRA_MODES:
-            EXTRA_MODES[k](args, torch, kv, W)
+            print(json.dumps(EXTRA_MODES[k](args, torch, kv, W)), flush=True)
         else:
-            run_single(args, torch, kv, W, k)
+            print(json.dumps(run_single(args, torch, kv, W, k)), flush=True)
     finally:
         close_io_stream(torch, kv)
 
@@ -1603,9 +1802,11 @@ def run_single(args, torch, kv, W, k):
     if steady:
         result["steady_state"] = steady
     pool.close()
+    del pool_t
     host.free()
     out.free()
-    print(json.dumps(result), flush=True)
+    torch.cuda.empty_cache()
+    return result
 
 
 if __name__ == "__main__":

@@ -103,3 +103,54 @@ def test_peak_report_keeps_an_unmeasured_bidirectional_peak():
     assert r["bidir"] is None and r["bidir_note"] == note
     # the roofline of the bidirectional workload then has no measured ceiling
     assert bench.roofline("k", 88.0, r["bidir"], directions=2)["frac_of_measured_peak"] is None
+
+
+def test_measured_traffic_averages_over_launches(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_2508_18572_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    (csrc / "kvio_kernels.hip").write_bytes(b"kernel")
+    (csrc / "kvio_internal.h").write_bytes(b"header")
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    hashes = " ".join(hashlib.sha256(x).hexdigest() for x in (b"kernel", b"header"))
+    (prof / bench.COUNTER_FILES[4]).write_text(
+        f"kernel_sources_sha256: {hashes}\nload_launches: 4\nload_fetch_kib: 400.0\nload_write_kib: 800.0\n"
+        "fetch_scale: 2.0\nwrite_scale: 1.0\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    t = bench.measured_traffic(4, True)
+    assert t["fetch_bytes"] == 200 * 1024 and t["write_bytes"] == 200 * 1024
+
+
+def test_cpu_baseline_batched_moves_what_it_counts():
+    """The batched CPU baseline runs the oracle on pieces of whole pages and
+    counts 2 x rows x R per piece and plane; its slab image ends up holding the
+    last plane's rows where the oracle puts them."""
+    import numpy as np
+
+    import oracle
+    L, R, P, S = 2, 64, 16, 32768
+    rng = np.random.default_rng(3)
+    hit = [1000, 20000, 37]
+    sizes = [L * 2 * h * R for h in hit]
+    chunk = rng.integers(0, 256, sum(sizes), dtype=np.uint8)
+    pages = rng.permutation(S // P).astype(np.int32)
+    spans, o, p0 = [], 0, 0
+    for h, b in zip(hit, sizes):
+        n = -(-h // P)
+        spans.append((o, h, h, pages[p0:p0 + n]))
+        o += b
+        p0 += n
+    for threads in (1, 3):
+        nb, el, planes = bench.cpu_baseline_batched(S, R, chunk, spans, P, L, 0.2, threads)
+        assert planes >= 1 and el > 0
+        assert nb % (2 * R) == 0 and nb >= 2 * R * sum(hit) * planes
+    # the same pieces through the oracle directly reproduce one plane's slab
+    exp = np.zeros((S, R), np.uint8)
+    for off, ht, nt, pg in spans:
+        oracle.load_slab(exp, P, chunk[off:off + nt * R], nt, pg)
+    slab = np.zeros((S, R), np.uint8)
+    for off, ht, nt, pg in spans:
+        for a in range(0, nt, 8192):
+            n = min(8192, nt - a)
+            oracle.load_slab(slab, P, chunk[off + a * R:off + (a + n) * R], n, pg[a // P:])
+    assert np.array_equal(slab, exp)
