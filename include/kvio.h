@@ -212,6 +212,28 @@ kvio_status kvio_offload(kvio_pool_t pool, const kvio_span *spans, int32_t n_spa
 kvio_status kvio_load_layer(kvio_pool_t pool, const kvio_span *spans, int32_t n_spans,
                             int32_t layer, hipStream_t stream, hipEvent_t done);
 
+/* For callers that cannot allocate -- code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc: kvio_load without a pool
+ * handle, allocating nothing (no hipMalloc, hipFree or other allocating
+ * call; no host-to-device copy).  `desc` describes the pool as for
+ * kvio_pool_create and is checked the same way on every call (staged loads,
+ * which need staging memory, are refused); spans, layer range, stream and
+ * result are those of kvio_load.  The device memory a pool handle would own
+ * -- the table of layer addresses and the error word -- lives in a static
+ * 4 KiB device array of the library (one per GPU, held until the process
+ * ends), so the call takes at most KVIO_NOALLOC_MAX_LAYERS layers and at most
+ * KVIO_MAX_SPANS_PER_LAUNCH spans (KVIO_EINVAL beyond either).  Each call
+ * first enqueues a one-workgroup kernel that writes the layer table and
+ * clears the error word, then the load kernel.  Every call on a GPU shares
+ * that array: calls that overlap on one GPU (on different streams, or from
+ * different threads) race and must be ordered by the caller.  A page index
+ * outside [0, S / P) is skipped, never dereferenced, and not reported (use a
+ * pool handle and kvio_check to diagnose one).  n_spans == 0 or all
+ * num_tokens == 0 enqueues nothing. */
+#define KVIO_NOALLOC_MAX_LAYERS 128
+kvio_status kvio_load_noalloc(const kvio_pool_desc *desc, const kvio_span *spans, int32_t n_spans,
+                              int32_t layer_begin, int32_t layer_end, hipStream_t stream);
+
 /* The library's own error reporting; no passage of the paper defines it.
  * Synchronise the device, then report and clear the device error record:
  * KVIO_ERANGE (with the span and context page in kvio_last_error) if an

@@ -14,4 +14,5 @@ from .kvio import (  # noqa: F401
     kvio_pool_destroy, kvio_span, kvio_strerror, launch, make_spans, Stream,
     kvio_stream_create, kvio_stream_destroy, kvio_schedule_round, kvio_disk_prefetch, kvio_disk_store_pages, DiskPrefetch,
     KVIO_DISK_PAGE_FIRST, KVIO_DISK_LAYER_FIRST, KVIO_EIO,
+    KVIO_NOALLOC_MAX_LAYERS, kvio_load_noalloc, pool_desc,
 )

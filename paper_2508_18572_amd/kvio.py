@@ -50,6 +50,7 @@ KVIO_DISK_LAYER_FIRST = 1
 KVIO_HOST_COHERENT = 0x0
 KVIO_HOST_NONCOHERENT = 0x1
 KVIO_MAX_SPANS_PER_LAUNCH = 64
+KVIO_NOALLOC_MAX_LAYERS = 128
 
 
 class kvio_launch(ctypes.Structure):
@@ -122,6 +123,7 @@ def _load_library() -> ctypes.CDLL:
                                      ctypes.POINTER(vp)],
         "kvio_disk_prefetch_progress": [vp, ctypes.POINTER(i32)],
         "kvio_disk_prefetch_finish": [vp, i32, ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(i32)],
+        "kvio_load_noalloc": [ctypes.POINTER(kvio_pool_desc), ctypes.POINTER(kvio_span), i32, i32, i32, vp],
         "kvio_schedule_round": [ctypes.POINTER(kvio_request), i32, ctypes.POINTER(kvio_batch_policy),
                                 ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32),
                                 ctypes.POINTER(i32)],
@@ -144,7 +146,7 @@ EXPORTS = ("kvio_pool_create", "kvio_pool_destroy", "kvio_load", "kvio_offload",
            "kvio_check", "kvio_naive_load", "kvio_naive_offload", "kvio_memcpy", "kvio_host_alloc",
            "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_schedule_round",
            "kvio_disk_prefetch", "kvio_disk_store_pages", "kvio_disk_prefetch_start", "kvio_disk_prefetch_progress",
-           "kvio_disk_prefetch_finish",
+           "kvio_disk_prefetch_finish", "kvio_load_noalloc",
            "kvio_strerror", "kvio_last_error")
 
 
@@ -208,15 +210,34 @@ def kvio_pool_create(num_layers: int, num_kv_heads: int, head_dim: int, elem_byt
                      offload_launch: Optional[kvio_launch] = None,
                      host_layout: int = KVIO_HOST_TOKEN_MAJOR, staging_bytes: int = 0) -> int:
     """Create a pool handle; k_layers / v_layers are device pointers (ints)."""
+    d, _keep = pool_desc(num_layers, num_kv_heads, head_dim, elem_bytes, page_size, num_slots, k_layers, v_layers,
+                         load_launch, offload_launch, host_layout, staging_bytes)
+    h = ctypes.c_void_p()
+    _check(_lib.kvio_pool_create(ctypes.byref(d), ctypes.byref(h)))
+    return h.value
+
+
+def pool_desc(num_layers: int, num_kv_heads: int, head_dim: int, elem_bytes: int, page_size: int,
+              num_slots: int, k_layers: Sequence[int], v_layers: Sequence[int],
+              load_launch: Optional[kvio_launch] = None, offload_launch: Optional[kvio_launch] = None,
+              host_layout: int = KVIO_HOST_TOKEN_MAJOR, staging_bytes: int = 0):
+    """A kvio_pool_desc; returns (desc, keep), where `keep` holds the pointer
+    arrays the description points into (keep it alive while desc is used)."""
     kt = (ctypes.c_void_p * len(k_layers))(*k_layers)
     vt = (ctypes.c_void_p * len(v_layers))(*v_layers)
     d = kvio_pool_desc(num_layers, num_kv_heads, head_dim, elem_bytes, page_size, host_layout,
                        num_slots, ctypes.cast(kt, ctypes.POINTER(ctypes.c_void_p)),
                        ctypes.cast(vt, ctypes.POINTER(ctypes.c_void_p)),
                        load_launch or kvio_launch(), offload_launch or kvio_launch(), staging_bytes)
-    h = ctypes.c_void_p()
-    _check(_lib.kvio_pool_create(ctypes.byref(d), ctypes.byref(h)))
-    return h.value
+    return d, (kt, vt)
+
+
+def kvio_load_noalloc(desc: "kvio_pool_desc", spans: Iterable[SpanLike], layer_begin: int, layer_end: int,
+                      stream=None) -> None:
+    """kvio_load from a pool description, allocating nothing (static device
+    scratch shared by every call on a GPU)."""
+    arr, n = make_spans(spans)
+    _check(_lib.kvio_load_noalloc(ctypes.byref(desc), arr, n, layer_begin, layer_end, _stream(stream)))
 
 
 def kvio_pool_destroy(pool: int) -> None:

@@ -83,6 +83,29 @@ def test_host_side_validation_without_device():
     assert lib.kvio_stream_destroy(None) == kv.KVIO_EINVAL
 
 
+def test_noalloc_argument_checks_without_device():
+    """kvio_load_noalloc refuses what its static table cannot hold before it
+    touches the device."""
+    import paper_2508_18572_amd as kv
+    desc, keep = kv.pool_desc(kv.KVIO_NOALLOC_MAX_LAYERS + 1, 4, 64, 2, 16, 4096, [16] * 129, [16] * 129)
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_load_noalloc(desc, [], 0, 1)
+    assert e.value.status == kv.KVIO_EINVAL and "layers exceed" in e.value.detail
+    desc, keep = kv.pool_desc(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16],
+                              load_launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED))
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_load_noalloc(desc, [], 0, 2)
+    assert e.value.status == kv.KVIO_EINVAL and "staged" in e.value.detail
+    desc, keep = kv.pool_desc(2, 3, 5, 2, 16, 4096, [16, 16], [16, 16])     # R = 30 B
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_load_noalloc(desc, [], 0, 2)
+    assert e.value.status == kv.KVIO_EALIGN
+    desc, keep = kv.pool_desc(2, 4, 64, 2, 16, 4096, [16, 16], [16, 16])
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_load_noalloc(desc, [(0, 0, 0, 0)] * (kv.KVIO_MAX_SPANS_PER_LAUNCH + 1), 0, 2)
+    assert e.value.status == kv.KVIO_EINVAL
+
+
 def test_package_refuses_to_import_without_the_library(tmp_path):
     """No fallback: without libkvio.so the package raises at import."""
     import shutil
