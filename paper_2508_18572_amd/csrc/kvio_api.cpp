@@ -469,17 +469,16 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
     kvio_status st = kvio::validate_spans(p->g, spans, n, l0, l1, fn, rs.data());
     if (st != KVIO_OK) return st;
     kvio_launch lc = dir == kvio::kLoad ? p->load_launch : p->offload_launch;
+    int64_t bytes = 0;                       // payload of the whole call
+    for (const Resolved &r : rs) bytes += r.num_tokens;
+    bytes *= 2 * int64_t(l1 - l0) * p->g.row_bytes;
     if (lc.flags & KVIO_LAUNCH_STAGED) {
-        int64_t bytes = 0;
-        for (const Resolved &r : rs) bytes += r.num_tokens;
-        bytes *= 2 * int64_t(l1 - l0) * p->g.row_bytes;
         if (bytes >= std::min(kStagedMinBytes, p->slot_bytes))
             return run_staged(p, rs, spans, n, l0, l1, stream, dir,
                               kvio::kernel_shape(p->g, lc, kvio::kDefaultStaged), fn);
         lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
     }
-    const kvio::Shape shape =
-        kvio::kernel_shape(p->g, lc, dir == kvio::kLoad ? kvio::kDefaultLoad : kvio::kDefaultOffload);
+    const kvio::Shape shape = kvio::kernel_shape(p->g, lc, kvio::default_shape(dir, bytes));
     return kvio::launch_spans(p->g, p->d_layers, p->d_err, rs.data(), n, l0, l1, dir, shape, stream, fn);
 }
 

@@ -63,13 +63,27 @@ struct Shape {
 };
 
 // Library defaults for the launch shape, chosen by measurement on MI355X
-// (PCIe Gen5 x16 host link).  Load: 16 workgroups x 4 waves with 4 KiB steps
-// saturate the link (57.6 GB/s at page size 1, the contiguous memcpy peak),
-// reach 90% of it on a 2 MiB context, and leave 240 of 256 CUs to co-running
-// compute.  Offload: 32 workgroups x 4 waves with 16 KiB steps (55.6 GB/s).
+// (PCIe Gen5 x16 host link), on 16 of the 256 CUs for loads.
+//   Load of 32 MiB or more: 16 workgroups x 3 waves, 4 KiB steps (192 KiB in
+//   flight).  That saturates the link alone (57.6 GB/s at page size 1, the
+//   contiguous memcpy peak) and, beside an offload running on a small quota,
+//   leaves the offload's writes room on the link: 97.9 GB/s both ways
+//   against 88.6 GB/s with 4 waves per workgroup, whose extra outstanding
+//   reads slow both directions.
+//   Smaller loads: 16 x 4 waves.  A 2 MiB context is 512 tiles of 4 KiB,
+//   which 64 waves share evenly (8 each) and finish ~1 us sooner than 48.
+//   Offload: 32 workgroups x 4 waves with 16 KiB steps (55.7 GB/s).
 constexpr int kDefaultThreads = 256;
-constexpr Shape kDefaultLoad = {16, kDefaultThreads, 4, true, true};
+constexpr Shape kDefaultLoad = {16, 192, 4, true, true};
+constexpr Shape kDefaultLoadSmall = {16, kDefaultThreads, 4, true, true};
+constexpr int64_t kSmallLoadBytes = int64_t(32) << 20;
 constexpr Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
+
+// The default shape of a call that moves `bytes` in direction `dir`.
+inline Shape default_shape(int dir, int64_t bytes) {
+    if (dir != 0) return kDefaultOffload;
+    return bytes < kSmallLoadBytes ? kDefaultLoadSmall : kDefaultLoad;
+}
 // Staged transfers: the scatter / gather between the HBM staging buffer and
 // the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at
 // page size 1 in 1.75 ms, 2.4 TB/s of payload).

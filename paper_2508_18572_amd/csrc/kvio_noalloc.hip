@@ -92,9 +92,9 @@ extern "C" kvio_status kvio_load_noalloc(const kvio_pool_desc *desc, const kvio_
     kvio::Resolved rs[KVIO_MAX_SPANS_PER_LAUNCH];
     st = kvio::validate_spans(g, spans, n_spans, layer_begin, layer_end, fn, rs);
     if (st != KVIO_OK) return st;
-    bool any = false;
-    for (int32_t i = 0; i < n_spans; ++i) any = any || rs[i].num_tokens > 0;
-    if (!any) return KVIO_OK;                     // nothing to move: nothing enqueued
+    int64_t tokens = 0;
+    for (int32_t i = 0; i < n_spans; ++i) tokens += rs[i].num_tokens;
+    if (tokens == 0) return KVIO_OK;              // nothing to move: nothing enqueued
     uint8_t *base = nullptr;
     st = scratch_address(fn, &base);
     if (st != KVIO_OK) return st;
@@ -103,7 +103,9 @@ extern "C" kvio_status kvio_load_noalloc(const kvio_pool_desc *desc, const kvio_
     hipLaunchKernelGGL(kvio_noalloc_setup, dim3(1), dim3(256), 0, stream, init);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return kvio::fail_hip(e, fn);
-    const kvio::Shape shape = kvio::kernel_shape(g, desc->load_launch, kvio::kDefaultLoad);
+    const kvio::Shape shape = kvio::kernel_shape(
+        g, desc->load_launch,
+        kvio::default_shape(kvio::kLoad, tokens * 2 * (layer_end - layer_begin) * g.row_bytes));
     return kvio::launch_spans(g, init.table, init.err, rs, n_spans, layer_begin, layer_end, kvio::kLoad, shape,
                               stream, fn);
 }
