@@ -917,8 +917,10 @@ def run_bidirectional(args, torch, kv, W):
     res.update({
         "tokens_per_s": round((T + n_in * TO) / (t_load * 1e-3), 1),
         "load": {"gbps_concurrent": round(load_gbps, 3), "gbps_alone": round(nb / (t_load_alone * 1e-3) / GB, 3),
+                 "frac_of_h2d_peak_concurrent": round(load_gbps / peak["h2d"], 4) if peak else None,
                  "frac_of_h2d_peak_alone": round(nb / (t_load_alone * 1e-3) / GB / peak["h2d"], 4) if peak else None},
         "offload": {"gbps_concurrent": round(off_gbps, 3), "runs_in_window": n_in,
+                    "frac_of_d2h_peak_concurrent": round(off_gbps / peak["d2h"], 4) if peak else None,
                     "gbps_alone": round(nbo / (t_off_alone * 1e-3) / GB, 3),
                     "frac_of_d2h_peak_alone": round(nbo / (t_off_alone * 1e-3) / GB / peak["d2h"], 4) if peak else None},
         "bidirectional_gbps": round(bidir, 3),
@@ -1577,7 +1579,10 @@ def run_other_workloads(args, torch, kv, W):
     out["workload_5"] = {
         "workload": r["config"]["workload"], "reps": r["reps"], "bidirectional_gbps": r["bidirectional_gbps"],
         "frac_of_bidir_peak": r["frac_of_bidir_peak"], "load_gbps_concurrent": r["load"]["gbps_concurrent"],
-        "offload_gbps_concurrent": r["offload"]["gbps_concurrent"], "load_gbps_alone": r["load"]["gbps_alone"],
+        "offload_gbps_concurrent": r["offload"]["gbps_concurrent"],
+        "load_frac_of_h2d_peak_concurrent": r["load"]["frac_of_h2d_peak_concurrent"],
+        "offload_frac_of_d2h_peak_concurrent": r["offload"]["frac_of_d2h_peak_concurrent"],
+        "load_gbps_alone": r["load"]["gbps_alone"],
         "offload_gbps_alone": r["offload"]["gbps_alone"]}
     return out
 
