@@ -91,8 +91,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--interference", action="store_true",
                     help="resource-quota sweep (Strata Fig. 5 analogue): load GB/s and the slowdown of a "
-                         "co-running prefill-like GEMM and decode-like HBM-bound kernel vs. the load's "
-                         "workgroup quota, on the Llama-3.1-8B page-size-1 workload")
+                         "co-running Llama-3.1-8B prefill pass (2 x 4K tokens) or decoding step (16 x 4K) vs. "
+                         "the load's quota and CU placement, on the Llama-3.1-8B page-size-1 workload")
     ap.add_argument("--page-sweep", action="store_true",
                     help="Llama-3.1-8B KV: kvio vs one hipMemcpyAsync per page segment over page sizes "
                          "1..256 (32K tokens), plus 8192 tokens at page size 32")
@@ -383,6 +383,52 @@ def steady_state(torch, kv, pool, span, host, stream, payload, reps):
     out["single_shot_us"] = out["load_single_shot_wall_us"]
     out["reps"] = reps
     del dev
+    return out
+
+
+def launch_breakdown(torch, kv, pool, span, page_span, page_bytes, payload, h2d_peak, n=200):
+    """Where the time of a small load goes.  Three chains of n launches are
+    captured in HIP graphs (torch.cuda.CUDAGraph) and replayed, so the host
+    never gates the GPU: the whole small context, a single page of it, and a
+    one-element torch kernel.  Per launch: the empty kernel gives the GPU's
+    launch-to-launch cost, the one-page load adds the host link's first-byte
+    latency, and the rest of the small context's time is streaming, compared
+    with its bytes at the measured H2D peak."""
+    s = torch.cuda.Stream()
+    x = torch.zeros(1, device="cuda")
+    chains = {"context": lambda: pool.load(span, stream=s), "page": lambda: pool.load(page_span, stream=s),
+              "empty_kernel": lambda: x.add_(1.0)}
+    out = {}
+    for name, fn in chains.items():
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(n):
+                fn()
+        ts = []
+        with torch.cuda.stream(s):                      # replay() launches on the current stream
+            g.replay()
+            torch.cuda.synchronize()
+            for _ in range(5):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(s)
+                g.replay()
+                b.record(s)
+                torch.cuda.synchronize()
+                ts.append(a.elapsed_time(b) * 1e3 / n)
+        out[f"{name}_us_per_launch"] = round(statistics.median(ts), 3)
+        del g
+    pool.check()
+    if h2d_peak:
+        stream_us = payload / (h2d_peak * GB) * 1e6
+        out["context_at_h2d_peak_us"] = round(stream_us, 3)
+        out["page_bytes"] = page_bytes
+        out["first_byte_us"] = round(out["page_us_per_launch"] - out["empty_kernel_us_per_launch"]
+                                     - page_bytes / (h2d_peak * GB) * 1e6, 3)
+        out["context_minus_streaming_us"] = round(out["context_us_per_launch"] - stream_us, 3)
     return out
 
 
@@ -940,16 +986,85 @@ def run_bidirectional(args, torch, kv, W):
     return res
 
 
-def run_interference(args, torch, kv, W):
-    """Load bandwidth and co-runner slowdown vs. the load kernel's quota.
+class Fig5Corunners:
+    """The co-runners of the paper's interference experiment (Fig. 5), on the
+    Llama-3.1-8B shape (32 layers, hidden 4096, 32 query / 8 KV heads of 128,
+    MLP 14336), bf16, random weights, one set per layer:
 
-    Stand-ins for the paper's co-runners (Fig. 5): a prefill-like bf16 GEMM
-    (two 4K-token requests through a Llama-3.1-8B MLP up-projection,
-    8192 x 4096 x 14336) and a decode-like HBM-bound pass (reading the KV of 16
-    requests x 4K tokens of the 8B shape, 8 GiB, as one reduction).  The
-    co-runner loops on its own stream while one 4 GiB kvio_load runs on the
-    transfer stream; iterations that lie inside the load's window give the
-    co-run time per iteration."""
+      prefill: one forward pass over 2 requests x 4K tokens (8192 rows): per
+               layer the QKV projection (8192 x 4096 x 6144), the output
+               projection (8192 x 4096 x 4096), gate and up together
+               (8192 x 4096 x 28672) and down (8192 x 14336 x 4096), in order;
+      decode:  one decoding step of 16 requests with 4K-token contexts: per
+               layer the same four projections at 16 rows, and attention
+               reading the layer's K and V of the 16 x 4096 tokens (128 MiB
+               each) as two batched products.
+
+    Attention inside the prefill pass (about 8% of its FLOPs at 4K) is left
+    out; every product has contiguous operands."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        L, Hd, I, KVd = 32, 4096, 14336, 1024
+        g = torch.Generator(device="cuda").manual_seed(55)
+        bf = torch.bfloat16
+
+        def r(*shape):
+            return torch.randn(*shape, device="cuda", dtype=bf, generator=g).mul_(0.02)
+
+        self.layers = [(r(Hd, Hd + 2 * KVd), r(Hd, Hd), r(Hd, 2 * I), r(I, Hd)) for _ in range(L)]
+        self.x = r(8192, Hd)
+        self.qkv = torch.empty(8192, Hd + 2 * KVd, device="cuda", dtype=bf)
+        self.o = r(8192, Hd)
+        self.gu = torch.empty(8192, 2 * I, device="cuda", dtype=bf)
+        self.h = r(8192, I)
+        self.y = torch.empty(8192, Hd, device="cuda", dtype=bf)
+        self.xd = r(16, Hd)
+        self.dq = torch.empty(16, Hd + 2 * KVd, device="cuda", dtype=bf)
+        self.do = r(16, Hd)
+        self.dgu = torch.empty(16, 2 * I, device="cuda", dtype=bf)
+        self.dh = r(16, I)
+        self.dy = torch.empty(16, Hd, device="cuda", dtype=bf)
+        self.kcache = [r(16, 4096, KVd) for _ in range(L)]
+        self.vcache = [r(16, 4096, KVd) for _ in range(L)]
+        self.q = r(16, KVd, 4)
+        self.p = r(16, 4, 4096)
+        self.s = torch.empty(16, 4096, 4, device="cuda", dtype=bf)
+        self.a = torch.empty(16, 4, KVd, device="cuda", dtype=bf)
+        self.flop = {"prefill": 2.0 * 8192 * L * (Hd * (Hd + 2 * KVd) + Hd * Hd + Hd * 2 * I + I * Hd)}
+
+    def prefill(self):
+        mm = self.torch.matmul
+        for wqkv, wo, wgu, wd in self.layers:
+            mm(self.x, wqkv, out=self.qkv)
+            mm(self.o, wo, out=self.y)
+            mm(self.x, wgu, out=self.gu)
+            mm(self.h, wd, out=self.y)
+
+    def decode(self):
+        mm, bmm = self.torch.matmul, self.torch.bmm
+        for (wqkv, wo, wgu, wd), kc, vc in zip(self.layers, self.kcache, self.vcache):
+            mm(self.xd, wqkv, out=self.dq)
+            bmm(kc, self.q, out=self.s)
+            bmm(self.p, vc, out=self.a)
+            mm(self.do, wo, out=self.dy)
+            mm(self.xd, wgu, out=self.dgu)
+            mm(self.dh, wd, out=self.dy)
+
+
+def run_interference(args, torch, kv, W):
+    """Load bandwidth and co-runner slowdown against the load's quota and
+    placement (the paper's Fig. 5 on the kernel path).  The co-runners are a
+    prefill pass and a decoding step of the Llama-3.1-8B shape
+    (Fig5Corunners).  A co-runner repeats its pass on its own stream while
+    4 GiB loads of the Llama-3.1-8B KV (page size 1, 32K tokens into random
+    slots) run back to back on the transfer stream; the passes that lie wholly
+    inside the loads' window give the co-run time per pass, against the
+    faster of its median alone before and after the sweep.
+
+    Placements: every quota runs unmasked (the dispatcher places the load's
+    workgroups); the masked rows put the load on a stream limited to the
+    first n CUs and the co-runner on a stream limited to the others."""
     k = 2
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -963,19 +1078,11 @@ def run_interference(args, torch, kv, W):
     W.fill_cuda(host.ptr, nb, W.data_seed(k), shp)
     io, comp = io_stream(torch, kv), torch.cuda.Stream()
     span = [(host.ptr, T, T, pidx.data_ptr())]
-    g = torch.Generator(device="cuda").manual_seed(7)
-    A = torch.randn(8192, 4096, device="cuda", dtype=torch.bfloat16, generator=g)
-    B = torch.randn(4096, 14336, device="cuda", dtype=torch.bfloat16, generator=g)
-    C = torch.empty(8192, 14336, device="cuda", dtype=torch.bfloat16)
-    kvbuf = torch.randn(4 << 30, device="cuda", dtype=torch.bfloat16, generator=g)   # 8 GiB
-    red = torch.empty((), device="cuda", dtype=torch.float32)
-    corunners = {
-        "prefill_gemm": lambda: torch.matmul(A, B, out=C),
-        "decode_hbm": lambda: torch.sum(kvbuf, dim=(0,), dtype=torch.float32, out=red),
-    }
+    co = Fig5Corunners(torch)
+    corunners = {"prefill": co.prefill, "decode": co.decode}
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
 
-    def alone(fn, n=20, stream=None):
-        stream = comp if stream is None else stream
+    def alone(fn, n, stream):
         ts = []
         for _ in range(n):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -987,8 +1094,7 @@ def run_interference(args, torch, kv, W):
         torch.cuda.synchronize()
         return statistics.median(x.elapsed_time(y) for x, y in ts)
 
-    def load_alone(pool, stream=None):
-        stream = io if stream is None else stream
+    def load_alone(pool, stream):
         pool.load(span, stream=stream)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -996,100 +1102,102 @@ def run_interference(args, torch, kv, W):
         pool.load(span, stream=stream)
         b.record(stream)
         torch.cuda.synchronize()
-        return a.elapsed_time(b)
+        return nb / (a.elapsed_time(b) * 1e-3) / GB
 
-    def corun(pool, fn, n_iter, io_s, comp_s):
-        """The co-runner loops on comp_s while one load runs on io_s: load GB/s
-        and the median co-runner iteration inside the load's window."""
+    def corun(pool, fn, t_alone, io_s, comp_s):
+        """Passes of fn on comp_s beside back-to-back loads on io_s covering
+        at least 3 passes (and 150 ms): load GB/s over the loads' window and
+        the median pass inside it."""
+        n_loads = max(2, int(max(3 * t_alone, 150.0) / 75.0) + 1)
+        n_pass = int(n_loads * 75.0 / t_alone) + 4
         torch.cuda.synchronize()
         start = torch.cuda.Event(enable_timing=True)
         start.record(comp_s)
         marks = []
         with torch.cuda.stream(comp_s):
-            for _ in range(n_iter):
+            for _ in range(n_pass):
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a.record(comp_s)
                 fn()
                 b.record(comp_s)
                 marks.append((a, b))
-        io_s.wait_event(marks[5][0])                        # the co-runner is already running
+        io_s.wait_event(marks[1][0])                        # the co-runner is already running
         l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         l0.record(io_s)
-        pool.load(span, stream=io_s)
+        for _ in range(n_loads):
+            pool.load(span, stream=io_s)
         l1.record(io_s)
         torch.cuda.synchronize()
         t0, t1 = start.elapsed_time(l0), start.elapsed_time(l1)
         inside = [x.elapsed_time(y) for x, y in marks
                   if start.elapsed_time(x) >= t0 and start.elapsed_time(y) <= t1]
-        return round(nb / ((t1 - t0) * 1e-3) / GB, 3), (round(statistics.median(inside), 4) if inside else None)
+        return (round(n_loads * nb / ((t1 - t0) * 1e-3) / GB, 3),
+                round(statistics.median(inside), 4) if inside else None, len(inside))
 
-    quotas = [(1, 1024), (2, 1024), (4, 1024), (2, 256), (4, 256), (8, 256), (16, 256), (32, 256),
-              (64, 256), (128, 256), (32, 64), (64, 64), (128, 64), (256, 64), (64, 128), (128, 128),
-              ("staged", None)]
+    for fn in corunners.values():                       # warm the clocks and the GEMM heuristics
+        alone(fn, 5, comp)
+    base = {name: alone(fn, 10, comp) for name, fn in corunners.items()}
+    log("co-runners alone: " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()) +
+        f" (prefill {co.flop['prefill'] / (base['prefill'] * 1e-3) / 1e12:.0f} TFLOP/s)")
     rows = []
-    for fn in corunners.values():               # warm the clocks before the first baseline
-        alone(fn, 50)
-    base = {name: alone(fn) for name, fn in corunners.items()}
-    log(f"co-runners alone: " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
+    quotas = [(1, 1024), (2, 1024), (4, 1024), (8, 256), (8, 512), (8, 1024), (16, 192), (16, 256), (32, 64),
+              (64, 64)]
     for wg, th in quotas:
-        if wg == "staged":     # copy engine + HBM scatter at the default scatter shape
-            pool = kv.KVPool(pool_t, P, load_launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED),
-                             staging_bytes=args.staging_mib << 20)
-        else:
-            pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
-        row = {"workgroups": wg, "threads": th, "waves": wg * th // 64 if th else None,
-               "load_gbps_alone": round(nb / (load_alone(pool) * 1e-3) / GB, 3)}
+        pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
+        row = {"placement": "unmasked", "workgroups": wg, "threads": th, "waves": wg * th // 64,
+               "load_gbps_alone": round(load_alone(pool, io), 3)}
         for name, fn in corunners.items():
-            n_iter = int(200 / base[name]) + 20            # enough to outlast the load
-            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"] = corun(pool, fn, n_iter, io, comp)
+            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"], row[f"{name}_passes"] = corun(
+                pool, fn, base[name], io, comp)
         pool.close()
         rows.append(row)
-    # CU partitions: the load (default shape, 16 workgroups) on a stream masked
-    # to 16 CUs and the co-runner on a stream masked to the other CUs, so no CU
-    # holds both; the first 16 CUs, and every 16th CU.
-    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
-    for label, io_cus in (("cu_mask_first_16", list(range(16))),
-                          ("cu_mask_every_16th", list(range(0, n_cu, n_cu // 16))[:16])):
+        log(f"quota {wg} x {th}: " + ", ".join(f"{k2} {v}" for k2, v in row.items() if k2 not in ("workgroups",
+                                                                                                   "threads")))
+    # CU partitions: the load on a stream masked to the first n CUs (one workgroup
+    # per CU; 24 to 64 waves), the co-runner on a stream masked to the rest.
+    for n_io, (wg, th) in ((16, (16, 192)), (12, (12, 256)), (8, (8, 384)), (8, (8, 256)), (8, (8, 192)),
+                           (32, (32, 128))):
         try:
-            io_m = kv.Stream(io_cus)
+            io_m = kv.Stream(list(range(n_io)))
         except kv.KvioError as e:
-            log(f"{label}: masked stream refused ({e.detail})")
+            log(f"{n_io} CUs: masked stream refused ({e.detail})")
             continue
         try:
-            comp_m = kv.Stream([c for c in range(n_cu) if c not in io_cus])
+            comp_m = kv.Stream(list(range(n_io, n_cu)))
         except kv.KvioError as e:
-            log(f"{label}: masked stream refused ({e.detail})")
+            log(f"{n_io} CUs: masked stream refused ({e.detail})")
             io_m.close()
             continue
-        pool = kv.KVPool(pool_t, P)
-        row = {"workgroups": label, "threads": 256, "waves": 64,
-               "load_gbps_alone": round(nb / (load_alone(pool, io_m.torch) * 1e-3) / GB, 3)}
+        pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
+        row = {"placement": f"load on CUs 0-{n_io - 1}, co-runner on the other {n_cu - n_io}", "workgroups": wg,
+               "threads": th, "waves": wg * th // 64, "load_gbps_alone": round(load_alone(pool, io_m.torch), 3)}
         for name, fn in corunners.items():
-            row[f"{name}_ms_alone_on_{n_cu - 16}_cus"] = round(alone(fn, stream=comp_m.torch), 4)
-            n_iter = int(200 / base[name]) + 20
-            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"] = corun(pool, fn, n_iter, io_m.torch,
-                                                                          comp_m.torch)
+            row[f"{name}_ms_alone_on_{n_cu - n_io}_cus"] = round(alone(fn, 10, comp_m.torch), 4)
+            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"], row[f"{name}_passes"] = corun(
+                pool, fn, base[name], io_m.torch, comp_m.torch)
         pool.close()
         comp_m.close()
         io_m.close()
         rows.append(row)
-    # the baseline: the faster of the co-runner alone before and after the sweep
-    after = {name: alone(fn) for name, fn in corunners.items()}
+        log(f"masked {n_io}: " + ", ".join(f"{k2} {v}" for k2, v in row.items() if k2 != "placement"))
+    after = {name: alone(fn, 10, comp) for name, fn in corunners.items()}
     base = {n: min(base[n], after[n]) for n in base}
-    log(f"co-runners alone (best of before / after the sweep): " + ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
+    log("co-runners alone (best of before / after the sweep): " +
+        ", ".join(f"{n} {t:.3f} ms" for n, t in base.items()))
     for row in rows:
         for name in corunners:
             t = row[f"{name}_ms_corun"]
             row[f"{name}_slowdown"] = round(t / base[name], 4) if t else None
-        log(f"quota {row['workgroups']!s:>6} x {row['threads']!s:>4}: " + ", ".join(
-            f"{k2} {v}" for k2, v in row.items() if k2 not in ("workgroups", "threads")))
     res = base_result(args, max(r["load_gbps_alone"] for r in rows), 0.0,
-                      "interference sweep: Llama-3.1-8B KV, page size 1, 32K-token load into random slots",
-                      {"corunners": {"prefill_gemm": [8192, 4096, 14336], "decode_hbm_bytes": 8 << 30},
+                      "interference sweep (the paper's Fig. 5): 4 GiB Llama-3.1-8B KV loads beside a prefill "
+                      "pass (2 x 4K tokens) or a decoding step (16 x 4K) of the Llama-3.1-8B shape",
+                      {"corunners": {"prefill": "32 x [8192x4096x6144, 8192x4096x4096, 8192x4096x28672, "
+                                                "8192x14336x4096] bf16 GEMMs",
+                                     "decode": "32 x [16-row projections + K, V reads of 16 x 4096 tokens]"},
                        "corunner_ms_alone": {n: round(t, 4) for n, t in base.items()}})
     res["sweep"] = rows
     host.free()
-    print(json.dumps(res), flush=True)
+    return res
 
 
 def run_row_sweep(args, torch, kv, W):
@@ -1617,7 +1725,7 @@ def main():
         if not args.no_peak and not args.disk and not args.schedule:
             h2d_d2h_peak(torch, kv)
         if args.interference:
-            run_interference(args, torch, kv, W)
+            print(json.dumps(run_interference(args, torch, kv, W)), flush=True)
         elif args.disk:
             run_disk(args, torch, kv, W)
         elif args.page_sweep:
@@ -1750,6 +1858,8 @@ def run_single(args, torch, kv, W, k):
     if k == 1:
         steady = steady_state(torch, kv, pool, span_in, host, stream, payload, reps=1000)
         steady.update(small_context_pipelines(torch, kv, pool, host, T, P, S, pages, stream, payload))
+        steady["breakdown"] = launch_breakdown(torch, kv, pool, span_in, [(host.ptr, T, P, pidx.data_ptr())],
+                                               L * 2 * P * R, payload, peak["h2d"] if peak else None)
         if peak:   # the target is set against the steady state (a single 2 MiB shot is latency-bound)
             for key in ("load", "memcpy", "two_streams_load", "batched4_load"):
                 if f"{key}_gbps" in steady:
@@ -1758,6 +1868,7 @@ def run_single(args, torch, kv, W, k):
             f"{steady['single_shot_us']:.1f} us; same-size memcpy {steady['memcpy_gbps']:.2f} GB/s; "
             f"independent contexts on two streams {steady.get('two_streams_load_gbps')} GB/s, "
             f"four per batched call {steady.get('batched4_load_gbps')} GB/s")
+        log(f"launch breakdown (HIP graphs): {steady['breakdown']}")
 
     default_launch = not (args.workgroups or args.threads or args.tile_kib or args.cached or args.noncoherent_host
                           or args.no_lds or args.staged or args.host_layout != "token")
