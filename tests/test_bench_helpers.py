@@ -47,8 +47,10 @@ def test_committed_counters_match_the_kernel_sources():
     """Whether the committed counter summary names the current kernel sources
     (then the bench reports measured traffic; otherwise traffic is null until
     the counters are re-taken)."""
-    if bench.measured_traffic(2, True) is None:
-        pytest.skip("the committed counters were taken on other kernel sources: re-take them")
+    stale = [k for k in bench.COUNTER_FILES if bench.measured_traffic(k, True) is None]
+    if stale:
+        pytest.skip(f"the committed counters of workload(s) {stale} were taken on other kernel sources: "
+                    "re-take them")
 
 
 class _FakeKv:
