@@ -142,11 +142,14 @@ def _staging(slot_pages, P, R):
     return 0 if slot_pages == 0 else 4 * slot_pages * 2 * P * R + 48
 
 
-@pytest.mark.parametrize("slot_pages", [0, 1, 3, 10])
+@pytest.mark.parametrize("slot_pages", [1, 3, 10])
 def test_parity_staged(kv, slot_pages):
     """KVIO_LAUNCH_STAGED: copy-engine copies through HBM staging slots and a
     scatter / gather kernel.  Small slots split spans into units of whole
-    pages and cycle the four slots many times per call."""
+    pages and cycle the four slots many times per call.  Every call here
+    moves at least one slot's worth of rows, so it takes the staged path
+    (a staged call smaller than min(64 MiB, one slot) runs on the kernel
+    path; test_small_staged_calls_take_the_kernel_path)."""
     for flags in (kv.KVIO_LAUNCH_STAGED, kv.KVIO_LAUNCH_STAGED | kv.KVIO_LAUNCH_CACHED):
         launch = kv.launch(flags=flags)
         run_case(kv, 2, 8, 128, 16, 4096, [(1000, 1024), (333, 400), (0, 5), (17, 17)], launch=launch,
@@ -164,12 +167,24 @@ def test_parity_staged(kv, slot_pages):
 
 
 def test_parity_staged_many_spans(kv):
-    # 70 contexts: more units than one scatter launch carries
+    # 70 contexts: more units than one scatter launch carries (2-page slots, so the call is staged)
     rng = np.random.default_rng(19)
     spans = [(int(t), int(t) + int(e)) for t, e in zip(rng.integers(0, 40, 70), rng.integers(0, 3, 70))]
-    run_case(kv, 2, 8, 128, 16, 4096, spans, launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED), seed=19)
     run_case(kv, 2, 8, 128, 16, 4096, spans, launch=kv.launch(flags=kv.KVIO_LAUNCH_STAGED), seed=20,
              staging_bytes=_staging(2, 16, 2048))
+
+
+def test_small_staged_calls_take_the_kernel_path(kv):
+    """With the default 4 GiB of staging (1 GiB slots), calls that move less
+    than 64 MiB run on the kernel path in the default shape; the results are
+    the same.  These cases check that fallback, not the staged path."""
+    staged = kv.launch(flags=kv.KVIO_LAUNCH_STAGED)
+    rng = np.random.default_rng(19)
+    spans = [(int(t), int(t) + int(e)) for t, e in zip(rng.integers(0, 40, 70), rng.integers(0, 3, 70))]
+    run_case(kv, 2, 8, 128, 16, 4096, spans, launch=staged, seed=19)
+    run_case(kv, 2, 8, 128, 16, 4096, [(1000, 1024), (333, 400), (0, 5), (17, 17)], launch=staged, seed=40)
+    run_case(kv, 3, 8, 128, 1, 5000, [(1000, 1200), (1, 1)], l0=1, l1=3, launch=staged, seed=41)
+    run_case(kv, 1, 1, 8, 3, 300, [(70, 80), (5, 9)], launch=staged, seed=42)
 
 
 def test_staged_calls_keep_stream_order(kv):

@@ -166,3 +166,41 @@ def test_noalloc_rejects_what_it_cannot_hold(kv):
         kv.kvio_load_noalloc(big, [], 0, 1)
     assert e.value.status == kv.KVIO_EINVAL and "layers exceed" in e.value.detail
     torch.cuda.synchronize()
+
+
+def test_noalloc_load_replays_in_a_hip_graph(kv):
+    """The callers the entry point exists for capture it: a load captured into
+    a HIP graph (torch.cuda.CUDAGraph), replayed three times with new host
+    bytes and eager work between replays; every replay equals the oracle."""
+    import torch
+    L, H, D, P, S, T = 3, 8, 128, 16, 4096, 1000
+    R = H * D * 2
+    rng = np.random.default_rng(88)
+    pages = rng.permutation(S // P)[:-(-T // P)].astype(np.int32)
+    img = rng.integers(0, 256, size=(2, L, S, R), dtype=np.uint8)
+    pool_t = torch.from_numpy(img.view(np.uint16).reshape(2, L, S, H, D).copy()).cuda()
+    desc, keep_desc = kv.pool_desc(L, H, D, 2, P, S, [pool_t[0, l].data_ptr() for l in range(L)],
+                                   [pool_t[1, l].data_ptr() for l in range(L)])
+    pt = torch.from_numpy(pages).cuda()
+    with kv.HostBuffer(L * 2 * T * R) as hb:
+        hb.array[:] = 0
+        span = [(hb.ptr, T, T, pt.data_ptr())]
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        kv.kvio_load_noalloc(desc, span, 0, L, stream=s)          # warm-up outside the capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            kv.kvio_load_noalloc(desc, span, 0, L, stream=s)
+        exp = img.copy()
+        for rep in range(3):
+            print(f"[no_alloc] graph replay {rep}", flush=True)
+            W.fill_np(hb.array, 600 + rep, W.LLAMA8B)             # new bytes before each replay
+            g.replay()
+            torch.cuda.synchronize()
+            oracle.load(exp[0], exp[1], P, [(hb.array, T, T, pages)])
+            assert np.array_equal(_bytes(pool_t), exp), f"replay {rep}: pool differs from the oracle"
+            pool_t.view(torch.int16).add_(0)                      # eager work between replays
+            torch.cuda.synchronize()
+        del g
+    del keep_desc
