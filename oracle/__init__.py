@@ -219,3 +219,38 @@ def offload_layout(k_pool: np.ndarray, v_pool: np.ndarray, page_size: int, spans
     layer_end = k_pool.shape[0] if layer_end is None else layer_end
     _batch(_load().kvo_offload_layout, k_pool, v_pool, page_size, list(spans), layer_begin, layer_end,
            "offload_layout", layout, num_heads)
+
+
+def load_layout_layer(k_slab: np.ndarray, v_slab: np.ndarray, page_size: int, spans: Iterable[Span], layout: int,
+                      num_layers: int, layer: int, num_heads: int = 1) -> None:
+    """One layer of load_layout: loads layer `layer` of each span's chunk (a
+    context of num_layers layers in any layout) into the (S, R) K and V slab
+    images of that layer, in place.  The same C routine as load_layout, run
+    over the layer range [layer, layer + 1) with every layer's pool pointer
+    aimed at the two slabs; only `layer` is touched, so a whole-pool check can
+    build its expected image one layer at a time."""
+    assert k_slab.shape == v_slab.shape and k_slab.ndim == 2
+    for sl in (k_slab, v_slab):
+        assert sl.dtype == np.uint8 and sl.flags.c_contiguous
+    num_slots, row_bytes = k_slab.shape
+    spans = list(spans)
+    n = len(spans)
+    keep = []
+    hosts = (ctypes.c_void_p * max(n, 1))()
+    pidxs = (ctypes.c_void_p * max(n, 1))()
+    htok = np.zeros(max(n, 1), dtype=np.int64)
+    ntok = np.zeros(max(n, 1), dtype=np.int64)
+    for i, (host, host_tokens, num_tokens, page_idx) in enumerate(spans):
+        assert host.dtype == np.uint8 and host.flags.c_contiguous
+        assert host.size >= host_chunk_bytes(layout, num_layers, host_tokens, row_bytes, page_size)
+        p = np.ascontiguousarray(page_idx, dtype=np.int32)
+        keep.append(p)
+        hosts[i] = _ptr(host)
+        pidxs[i] = _ptr(p) if p.size else None
+        htok[i] = host_tokens
+        ntok[i] = num_tokens
+    kp = (ctypes.c_void_p * num_layers)(*([_ptr(k_slab)] * num_layers))
+    vp = (ctypes.c_void_p * num_layers)(*([_ptr(v_slab)] * num_layers))
+    rc = _load().kvo_load_layout(kp, vp, num_layers, num_slots, page_size, row_bytes, num_heads, layout, n, hosts,
+                                 _ptr(htok), _ptr(ntok), pidxs, layer, layer + 1)
+    _check(rc, "load_layout_layer")

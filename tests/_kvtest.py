@@ -209,3 +209,47 @@ def threaded_memset(ptr: int, byte: int, nbytes: int, threads: int = 16, chunk: 
 
     with ThreadPoolExecutor(threads) as ex:
         list(ex.map(one, range(0, nbytes, chunk)))
+
+
+def pool_matches_oracle_layout(pool_t, spans, page_size, layout, num_heads, workers=3):
+    """Whole-image parity of a load from chunks in any host layout (oracle
+    TOKEN_MAJOR / PAGE_FIRST / HEAD_MAJOR): layer by layer, the GPU pool's K and
+    V slabs equal, byte for byte, the oracle's load of that layer of `spans`
+    into slab images that hold the sentinel everywhere.  Returns the number of
+    slabs compared."""
+    import threading
+
+    import torch
+
+    import paper_2508_18572_amd as kvmod
+    _, L, S = pool_t.shape[:3]
+    R = pool_t[0, 0, 0].numel() * pool_t.element_size()
+    pool_b = pool_t.view(torch.uint8).view(2, L, S, R)
+    live = [(h, ht, nt, np.ascontiguousarray(p, np.int32)) for h, ht, nt, p in spans if nt > 0]
+    torch.cuda.synchronize()
+
+    def work(w):
+        errors = []
+        exp = [np.empty((S, R), np.uint8), np.empty((S, R), np.uint8)]
+        with kvmod.HostBuffer(S * R) as ik, kvmod.HostBuffer(S * R) as iv:
+            imgs = [ik, iv]
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                for l in range(w, L, workers):
+                    for kv in range(2):
+                        torch.from_numpy(imgs[kv].array).view(S, R).copy_(pool_b[kv, l])
+                        _libc.memset(exp[kv].ctypes.data, SENTINEL & 0xFF, S * R)
+                    stream.synchronize()
+                    oracle.load_layout_layer(exp[0], exp[1], page_size, live, layout, L, l, num_heads=num_heads)
+                    for kv in range(2):
+                        if _libc.memcmp(imgs[kv].ptr, exp[kv].ctypes.data, S * R) != 0:
+                            got = imgs[kv].array.reshape(S, R)
+                            errors.append(f"kv {kv} layer {l}: pool slab differs from the oracle "
+                                          f"(first row {_first_bad_row(got, exp[kv])})")
+        return errors
+
+    with ThreadPoolExecutor(workers) as ex:
+        errors = [m for errs in ex.map(work, range(workers)) for m in errs]
+    if errors:
+        raise AssertionError(f"{len(errors)} slab(s) differ: " + "; ".join(errors[:4]))
+    return 2 * L

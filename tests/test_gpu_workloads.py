@@ -21,8 +21,8 @@ import pytest
 
 import oracle
 import workloads as W
-from _kvtest import (SENTINEL, memequal, offload_matches_oracle, pool_matches_oracle, sampled_rows_match,
-                     threaded_memset, touched_mask, untouched_rows_hold_sentinel)
+from _kvtest import (SENTINEL, memequal, offload_matches_oracle, pool_matches_oracle, pool_matches_oracle_layout,
+                     sampled_rows_match, threaded_memset, touched_mask, untouched_rows_hold_sentinel)
 
 pytestmark = pytest.mark.gpu
 
@@ -135,6 +135,54 @@ def test_workload2_staged(kv, io_stream):
 def test_workload3_staged_layerwise(kv, io_stream):
     """Staged layer-wise loads of the 70B context (one slot per layer)."""
     single_context_workload(kv, 3, io_stream, layerwise=True, staged=True)
+
+
+@pytest.mark.parametrize("k,layout,layerwise", [(2, "head", False), (3, "page", True)],
+                         ids=["workload2_head_major", "workload3_page_first_layerwise"])
+def test_other_host_layouts_at_full_size(kv, io_stream, k, layout, layerwise):
+    """The head/token transpose (head-major chunks, through LDS) on workload 2
+    and the paper's page-first chunks on workload 3 loaded layer by layer, at
+    full size in the default launch shapes: the whole pool image against the
+    oracle's load of the same chunks, layer by layer, and the offload's round
+    trip back into a refilled chunk."""
+    import torch
+    wl = W.WORKLOADS[k]
+    shp = wl.shape
+    L, H, D, P, S, T = shp.num_layers, shp.num_kv_heads, shp.head_dim, wl.page_size, wl.num_slots, wl.tokens
+    R = shp.row_bytes
+    nbytes = L * 2 * T * R
+    hl = {"head": kv.KVIO_HOST_HEAD_MAJOR, "page": kv.KVIO_HOST_PAGE_FIRST}[layout]
+    ol = {"head": oracle.HEAD_MAJOR, "page": oracle.PAGE_FIRST}[layout]
+    rng = np.random.default_rng(W.placement_seed(k))
+    pages = W.random_slots(rng, S, T) if P == 1 else W.random_pages(rng, S // P, -(-T // P))
+    print(f"[workload{k} {layout}] L={L} S={S} T={T} R={R} layerwise {layerwise}", flush=True)
+    torch.cuda.empty_cache()
+    pool_t = new_pool(L, S, H, D, torch.bfloat16)
+    pt = torch.from_numpy(pages).cuda()
+    with kv.HostBuffer(nbytes) as hb, kv.HostBuffer(nbytes) as ob:
+        W.fill_cuda(hb.ptr, nbytes, W.data_seed(k) + 50, shp)
+        pool = kv.KVPool(pool_t, P, host_layout=hl)
+        span = [(hb.ptr, T, T, pt.data_ptr())]
+        if layerwise:
+            compute = torch.cuda.current_stream()
+            for l in range(L):
+                ev = torch.cuda.Event()
+                ev.record(io_stream)
+                pool.load_layer(span, l, stream=io_stream, done=ev)
+                compute.wait_event(ev)
+        else:
+            pool.load(span, stream=io_stream)
+        torch.cuda.synchronize()
+        pool.check()
+        assert pool_matches_oracle_layout(pool_t, [(hb.array, T, T, pages)], P, ol, H) == 2 * L
+        threaded_memset(ob.ptr, FILL, nbytes)
+        pool.offload([(ob.ptr, T, T, pt.data_ptr())], stream=io_stream)
+        torch.cuda.synchronize()
+        pool.check()
+        assert memequal(ob.ptr, hb.ptr, nbytes), "offload round trip differs from the host chunk"
+        pool.close()
+    del pool_t
+    torch.cuda.empty_cache()
 
 
 def batched_setup():

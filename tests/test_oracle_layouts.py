@@ -123,3 +123,25 @@ def test_page_first_requires_whole_pages():
     assert e.value.code == oracle.EINVAL
     with pytest.raises(oracle.OracleError):
         oracle.load_layout(pool[0], pool[1], P, [(host, 12, 12, np.arange(3, dtype=np.int32))], 7, num_heads=H)
+
+
+@pytest.mark.parametrize("L,H,De,P,S,T,N", [
+    (3, 4, 32, 4, 128, 32, 29),
+    (2, 8, 16, 16, 256, 64, 50),
+    (4, 1, 16, 1, 64, 24, 24),
+])
+def test_one_layer_at_a_time_equals_the_whole_load(L, H, De, P, S, T, N):
+    """load_layout_layer builds the expected pool one layer at a time; layer by
+    layer it must give exactly the slabs of load_layout (the numpy transpose of
+    the token-major chunk gives the other layouts' chunks, as above)."""
+    R = H * De
+    tm, pf, hm = chunks(L, T, H, De, P, seed=L * 7 + P)
+    pidx = np.random.default_rng(P + 1).permutation(S // P)[:-(-N // P)].astype(np.int32)
+    base = pool_of(L, S, R, seed=5)
+    for layout, chunk in ((oracle.TOKEN_MAJOR, tm), (oracle.PAGE_FIRST, pf), (oracle.HEAD_MAJOR, hm)):
+        whole = base.copy()
+        oracle.load_layout(whole[0], whole[1], P, [(chunk, T, N, pidx)], layout, num_heads=H)
+        for l in range(L):
+            k, v = base[0, l].copy(), base[1, l].copy()
+            oracle.load_layout_layer(k, v, P, [(chunk, T, N, pidx)], layout, L, l, num_heads=H)
+            assert np.array_equal(k, whole[0, l]) and np.array_equal(v, whole[1, l]), (layout, l)
