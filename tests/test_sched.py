@@ -152,3 +152,24 @@ def test_scheduler_under_sanitizers(tmp_path):
     run = subprocess.run([exe], capture_output=True, text=True, timeout=300)
     assert run.returncode == 0, run.stdout[-2000:] + run.stderr[-4000:]
     assert "scheduler fuzz checks passed" in run.stdout
+
+
+def test_ratio_boundary_is_exact_for_random_ratios(kv):
+    """At the boundary of the loading-bound test: with compute C in the batch,
+    a request loading floor(ratio * C) tokens (exact rational value of the
+    double `ratio`) is not loading-bound and one more token is.  Checked for
+    random ratios over many binary orders of magnitude and C up to 2^61."""
+    from fractions import Fraction
+    import random
+    rnd = random.Random(123)
+    for _ in range(400):
+        ratio = rnd.uniform(1.0, 2.0) * 2.0 ** rnd.randint(-40, 40)
+        c = rnd.randint(1, 2**61)
+        edge = Fraction(ratio) * c
+        tie = edge.numerator // edge.denominator
+        if tie + 1 >= 2**63 or tie < 1:
+            continue
+        for load, bound in ((tie, False), (tie + 1, True)):
+            q = [(0, c, -1, 0), (load, 0, -1, 0), (0, 1, -1, 0)]
+            got = run_both(kv, q, 2**63 - 1, 8, ratio=ratio)
+            assert got == (([0, 2, 1] if bound else [0, 1, 2]), []), (ratio, c, load)
