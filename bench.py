@@ -69,6 +69,9 @@ def parse():
     ap.add_argument("--other-reps", type=int, default=5,
                     help="timed repetitions of each other workload in the default run (reported as reps)")
     ap.add_argument("--no-other-workloads", action="store_true")
+    ap.add_argument("--swap", action="store_true",
+                    help="the batched workload swapped in both directions at once through two host buffers")
+    ap.add_argument("--swap-wave-gib", type=int, default=30, help="host bytes per wave of the swap (two buffers)")
     ap.add_argument("--workgroups", type=int, default=0)
     ap.add_argument("--threads", type=int, default=0)
     ap.add_argument("--tile-kib", type=int, default=0)
@@ -869,6 +872,102 @@ def run_batched(args, torch, kv, W):
     pool.close()
     del pool_t
     host.free()
+    torch.cuda.empty_cache()
+    return res
+
+
+def run_swap(args, torch, kv, W):
+    """The batched workload swapped through the link in both directions at
+    once: the 64 contexts of workload 4 move in waves of at most
+    --swap-wave-gib GiB (30 by default) through two host buffers, so wave w's offload (pool -> buffer w % 2, on its own
+    stream, with the background quota of --bg-offload) runs while wave w - 1
+    loads back (buffer (w - 1) % 2 -> pool, on the transfer stream).  A wave's
+    load waits for its offload; an offload into a buffer waits for the load
+    that last read it.  One step moves every context once in each direction;
+    set-up loads every wave first, as in the headline."""
+    k = 4
+    shp = W.LLAMA8B
+    L, H, D, P = shp.num_layers, shp.num_kv_heads, shp.head_dim, 16
+    R = shp.row_bytes
+    req = W.batched_requests(k)
+    S = req.pool_pages * P
+    hit = [int(h) for h in req.hit_tokens]
+    sizes = [L * 2 * h * R for h in hit]
+    waves = W.batch_waves(sizes, args.swap_wave_gib << 30)
+    total = sum(sizes)
+    wave_bytes = [sum(sizes[i] for i in w) for w in waves]
+    log(f"swap: {total / 2**30:.1f} GiB per direction in {len(waves)} waves through two host buffers")
+    peak = None if args.no_peak else h2d_d2h_peak(torch, kv)
+    torch.cuda.empty_cache()
+    pool_t = torch.empty((2, L, S, H, D), dtype=torch.bfloat16, device="cuda")
+    bg = [int(x) for x in args.bg_offload.split(",")]
+    pool = kv.KVPool(pool_t, P)
+    pool_off = kv.KVPool(pool_t, P, offload_launch=kv.launch(bg[0], bg[1], bg[2], 0))
+    pts = [torch.from_numpy(pl).cuda() for pl in req.page_lists]
+    bufs = [kv.HostBuffer(max(wave_bytes)), kv.HostBuffer(max(wave_bytes))]
+    sl, so = io_stream(torch, kv), torch.cuda.Stream()
+    spans = []
+    for j, w in enumerate(waves):
+        o, sp = 0, []
+        for i in w:
+            sp.append((bufs[j % 2].ptr + o, hit[i], hit[i], pts[i].data_ptr()))
+            o += sizes[i]
+        spans.append(sp)
+    for j, w in enumerate(waves):                          # set-up: every wave loaded once
+        o = 0
+        for i in w:
+            W.fill_cuda(bufs[j % 2].ptr + o, sizes[i], W.data_seed(k) * 1000 + i, shp)
+            o += sizes[i]
+        pool.load(spans[j], stream=sl)
+        torch.cuda.synchronize()
+    pool.check()
+
+    def step():
+        """Returns the events bracketing the step on the transfer stream."""
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(sl)
+        so.wait_event(e0)
+        loaded = [None, None]                             # last load that read each buffer
+        for j in range(len(waves)):
+            if loaded[j % 2] is not None:
+                so.wait_event(loaded[j % 2])
+            pool_off.offload(spans[j], stream=so)
+            off_done = torch.cuda.Event()
+            off_done.record(so)
+            sl.wait_event(off_done)
+            pool.load(spans[j], stream=sl)
+            ld = torch.cuda.Event()
+            ld.record(sl)
+            loaded[j % 2] = ld
+        e1 = torch.cuda.Event(enable_timing=True)
+        e1.record(sl)
+        return e0, e1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    marks = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    pool.check()
+    t_step = statistics.mean(a.elapsed_time(b) for a, b in marks)
+    value = 2 * total / (t_step * 1e-3) / GB
+    log(f"swap step {t_step:.1f} ms: {value:.2f} GB/s both directions")
+    res = base_result(args, value, t_step, "batched partial hits (workload 4) swapped in both directions at "
+                      "once: each wave's offload beside the previous wave's load, through two host buffers",
+                      {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "requests": len(hit),
+                       "tokens": sum(hit), "payload_bytes_per_direction": total, "waves": len(waves),
+                       "wave_payload_bytes": wave_bytes,
+                       "offload_launch": {"workgroups": bg[0], "threads": bg[1], "tile_kib": bg[2]}})
+    res.update({
+        "tokens_per_s": round(2 * sum(hit) / (t_step * 1e-3), 1),
+        "frac_of_bidir_peak": round(value / peak["bidir"], 4) if peak and peak["bidir"] else None,
+        "host_link_peak": peak_report(peak),
+    })
+    pool.close()
+    pool_off.close()
+    del pool_t
+    for b in bufs:
+        b.free()
     torch.cuda.empty_cache()
     return res
 
@@ -1728,6 +1827,8 @@ def main():
             print(json.dumps(run_interference(args, torch, kv, W)), flush=True)
         elif args.disk:
             run_disk(args, torch, kv, W)
+        elif args.swap:
+            print(json.dumps(run_swap(args, torch, kv, W)), flush=True)
         elif args.page_sweep:
             run_page_sweep(args, torch, kv, W)
         elif args.row_sweep:
