@@ -1188,7 +1188,11 @@ def run_interference(args, torch, kv, W):
 
     Placements: every quota runs unmasked (the dispatcher places the load's
     workgroups); the masked rows put the load on a stream limited to the
-    first n CUs and the co-runner on a stream limited to the others."""
+    first n CUs and the co-runner on a stream limited to the others.
+
+    Residency rows: one idle wave (torch's one-thread spin kernel, no memory
+    traffic) in place of the load, and the load with one one-wave workgroup
+    per CU (256 x 64), which leaves no CU without a resident wave."""
     k = 2
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -1231,9 +1235,22 @@ def run_interference(args, torch, kv, W):
     def corun(pool, fn, t_alone, io_s, comp_s):
         """Passes of fn on comp_s beside back-to-back loads on io_s covering
         at least 3 passes (and 150 ms): load GB/s over the loads' window and
-        the median pass inside it."""
+        the median pass inside it (None if no pass lies inside)."""
         n_loads = max(2, int(max(3 * t_alone, 150.0) / 75.0) + 1)
-        n_pass = int(n_loads * 75.0 / t_alone) + 4
+
+        def issue():
+            for _ in range(n_loads):
+                pool.load(span, stream=io_s)
+            return n_loads * nb
+
+        return corun_with(issue, n_loads * 75.0, fn, t_alone, io_s, comp_s)
+
+    def corun_with(issue, window_ms, fn, t_alone, io_s, comp_s):
+        """Passes of fn on comp_s while issue() runs on io_s (about window_ms
+        long): GB/s of the bytes issue() moved over its window, the median
+        pass inside the window, the number of such passes and the number of
+        passes that ended inside it (0 when the co-runner made no progress)."""
+        n_pass = int(window_ms / t_alone) + 4
         torch.cuda.synchronize()
         start = torch.cuda.Event(enable_timing=True)
         start.record(comp_s)
@@ -1248,15 +1265,15 @@ def run_interference(args, torch, kv, W):
         io_s.wait_event(marks[1][0])                        # the co-runner is already running
         l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         l0.record(io_s)
-        for _ in range(n_loads):
-            pool.load(span, stream=io_s)
+        moved = issue()
         l1.record(io_s)
         torch.cuda.synchronize()
         t0, t1 = start.elapsed_time(l0), start.elapsed_time(l1)
         inside = [x.elapsed_time(y) for x, y in marks
                   if start.elapsed_time(x) >= t0 and start.elapsed_time(y) <= t1]
-        return (round(n_loads * nb / ((t1 - t0) * 1e-3) / GB, 3),
-                round(statistics.median(inside), 4) if inside else None, len(inside))
+        ended = sum(1 for _, y in marks if t0 < start.elapsed_time(y) <= t1)
+        return (round(moved / ((t1 - t0) * 1e-3) / GB, 3),
+                round(statistics.median(inside), 4) if inside else None, len(inside), ended)
 
     for fn in corunners.values():                       # warm the clocks and the GEMM heuristics
         alone(fn, 5, comp)
@@ -1265,18 +1282,42 @@ def run_interference(args, torch, kv, W):
         f" (prefill {co.flop['prefill'] / (base['prefill'] * 1e-3) / 1e12:.0f} TFLOP/s)")
     rows = []
     quotas = [(1, 1024), (2, 1024), (4, 1024), (8, 256), (8, 512), (8, 1024), (16, 192), (16, 256), (32, 64),
-              (64, 64)]
+              (64, 64), (256, 64)]
     for wg, th in quotas:
         pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
         row = {"placement": "unmasked", "workgroups": wg, "threads": th, "waves": wg * th // 64,
                "load_gbps_alone": round(load_alone(pool, io), 3)}
         for name, fn in corunners.items():
-            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"], row[f"{name}_passes"] = corun(
-                pool, fn, base[name], io, comp)
+            (row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"], row[f"{name}_passes"],
+             row[f"{name}_passes_ended_in_window"]) = corun(pool, fn, base[name], io, comp)
         pool.close()
         rows.append(row)
         log(f"quota {wg} x {th}: " + ", ".join(f"{k2} {v}" for k2, v in row.items() if k2 not in ("workgroups",
                                                                                                    "threads")))
+    # One idle wave in place of the load: torch's spin kernel (one thread, no
+    # memory traffic) on the transfer stream, long enough for 5 passes alone
+    # (2 or more at the slowdown a resident load causes).
+    spin = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    spin[0].record(io)
+    with torch.cuda.stream(io):
+        torch.cuda._sleep(10_000_000)
+    spin[1].record(io)
+    torch.cuda.synchronize()
+    cycles_per_ms = 10_000_000 / spin[0].elapsed_time(spin[1])
+    row = {"placement": "one idle wave (spin kernel, no memory traffic) instead of the load", "workgroups": 1,
+           "threads": 1, "waves": 1, "load_gbps_alone": 0.0}
+    for name, fn in corunners.items():
+        window = max(5 * base[name], 150.0)
+
+        def idle(ms=window):
+            with torch.cuda.stream(io):
+                torch.cuda._sleep(int(ms * cycles_per_ms))
+            return 0
+
+        _, row[f"{name}_ms_corun"], row[f"{name}_passes"], row[f"{name}_passes_ended_in_window"] = corun_with(
+            idle, window, fn, base[name], io, comp)
+    rows.append(row)
+    log("idle wave: " + ", ".join(f"{k2} {v}" for k2, v in row.items() if k2 != "placement"))
     # CU partitions: the load on a stream masked to the first n CUs (one workgroup
     # per CU; 24 to 64 waves), the co-runner on a stream masked to the rest.
     for n_io, (wg, th) in ((16, (16, 192)), (12, (12, 256)), (8, (8, 384)), (8, (8, 256)), (8, (8, 192)),
@@ -1297,8 +1338,8 @@ def run_interference(args, torch, kv, W):
                "threads": th, "waves": wg * th // 64, "load_gbps_alone": round(load_alone(pool, io_m.torch), 3)}
         for name, fn in corunners.items():
             row[f"{name}_ms_alone_on_{n_cu - n_io}_cus"] = round(alone(fn, 10, comp_m.torch), 4)
-            row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"], row[f"{name}_passes"] = corun(
-                pool, fn, base[name], io_m.torch, comp_m.torch)
+            (row[f"load_gbps_with_{name}"], row[f"{name}_ms_corun"], row[f"{name}_passes"],
+             row[f"{name}_passes_ended_in_window"]) = corun(pool, fn, base[name], io_m.torch, comp_m.torch)
         pool.close()
         comp_m.close()
         io_m.close()
