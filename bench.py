@@ -205,13 +205,14 @@ class Timer:
 
 def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
     """Median GB/s of one contiguous pinned hipMemcpyAsync per direction (H2D from
-    src_ptr, D2H into dst_ptr), and of H2D and D2H running concurrently on two
+    src_ptr, D2H into dst_ptr), of the same copies by a plain kernel
+    (kvio_kernel_memcpy: the kernel path's own ceiling, keys kernel_h2d and
+    kernel_d2h), and of H2D and D2H memcpys running concurrently on two
     streams (each half the size)."""
     s1, s2 = io_stream(torch, kv), torch.cuda.Stream()
     half = nbytes // 2
     res = {}
-    for name, fn in (("h2d", lambda s: kv.kvio_memcpy(dev_ptr, src_ptr, nbytes, s)),
-                     ("d2h", lambda s: kv.kvio_memcpy(dst_ptr, dev_ptr, nbytes, s))):
+    def one_direction(name, fn):
         fn(s1)
         torch.cuda.synchronize()
         t = Timer(torch, s1)
@@ -221,6 +222,9 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
             t.stop(e)
         torch.cuda.synchronize()
         res[name] = nbytes / (statistics.median(t.ms()) * 1e-3) / GB
+
+    one_direction("h2d", lambda s: kv.kvio_memcpy(dev_ptr, src_ptr, nbytes, s))
+    one_direction("d2h", lambda s: kv.kvio_memcpy(dst_ptr, dev_ptr, nbytes, s))
     # bidirectional: H2D of one half while D2H of the other half.  Copies on
     # two ordinary streams can serialise (they may share a hardware queue);
     # a pair of the transfer stream (or the null stream) with a stream made
@@ -270,6 +274,8 @@ def memcpy_peak(torch, kv, src_ptr, dst_ptr, dev_ptr, nbytes, reps=5):
         res["bidir"] = None
         res["bidir_note"] = (f"unmeasured: the runtime serialised H2D and D2H copies on every stream pair "
                              f"tried in this process (best {best:.2f} GB/s)")
+    one_direction("kernel_h2d", lambda s: kv.kvio_kernel_memcpy(dev_ptr, src_ptr, nbytes, s))
+    one_direction("kernel_d2h", lambda s: kv.kvio_kernel_memcpy(dst_ptr, dev_ptr, nbytes, s))
     res["bytes"] = nbytes
     return res
 
@@ -526,7 +532,8 @@ def h2d_d2h_peak(torch, kv, nbytes=2 << 30):
             peak["bidir_note"] = ("measured in a fresh child process: this process's runtime serialised "
                                   "H2D and D2H copies on every stream pair tried")
     bidir = f"{peak['bidir']:.2f} GB/s" if peak["bidir"] else peak["bidir_note"]
-    log(f"memcpy peak: h2d {peak['h2d']:.2f} GB/s, d2h {peak['d2h']:.2f} GB/s, bidir {bidir}")
+    log(f"memcpy peak: h2d {peak['h2d']:.2f} GB/s, d2h {peak['d2h']:.2f} GB/s, bidir {bidir}; plain copy kernel: "
+        f"h2d {peak['kernel_h2d']:.2f} GB/s, d2h {peak['kernel_d2h']:.2f} GB/s")
     _PEAK["peak"] = peak
     return peak
 
@@ -878,10 +885,12 @@ def run_batched(args, torch, kv, W):
         "tokens_per_s": round(2 * sum(hit) / (t_step * 1e-3), 1),
         "load": {"gbps": round(load_gbps, 3), "ms_per_step": round(t_load, 3),
                  "tokens_per_s": round(sum(hit) / (t_load * 1e-3), 1),
-                 "frac_of_h2d_peak": round(load_gbps / peak["h2d"], 4) if peak else None},
+                 "frac_of_h2d_peak": round(load_gbps / peak["h2d"], 4) if peak else None,
+                 "frac_of_kernel_h2d_peak": round(load_gbps / peak["kernel_h2d"], 4) if peak else None},
         "offload": {"gbps": round(off_gbps, 3), "ms_per_step": round(t_off, 3),
                     "tokens_per_s": round(sum(hit) / (t_off * 1e-3), 1),
-                    "frac_of_d2h_peak": round(off_gbps / peak["d2h"], 4) if peak else None},
+                    "frac_of_d2h_peak": round(off_gbps / peak["d2h"], 4) if peak else None,
+                    "frac_of_kernel_d2h_peak": round(off_gbps / peak["kernel_d2h"], 4) if peak else None},
         "frac_of_host_link_peak": round((total / (peak["h2d"] * GB) + total / (peak["d2h"] * GB)) * 1e3 / t_step, 4)
         if peak else None,
         "wave_load_ms": [round(x, 3) for x in wave_load_ms],
@@ -1839,7 +1848,8 @@ def run_other_workloads(args, torch, kv, W):
         "workload": r["config"]["workload"], "reps": sub.steps, "step_gbps": r["value"],
         "ms_per_step": r["ms_per_step"], "load_gbps": r["load"]["gbps"],
         "load_frac_of_h2d_peak": r["load"]["frac_of_h2d_peak"], "offload_gbps": r["offload"]["gbps"],
-        "offload_frac_of_d2h_peak": r["offload"]["frac_of_d2h_peak"], "tokens_per_s": r["tokens_per_s"],
+        "offload_frac_of_d2h_peak": r["offload"]["frac_of_d2h_peak"],
+        "offload_frac_of_kernel_d2h_peak": r["offload"]["frac_of_kernel_d2h_peak"], "tokens_per_s": r["tokens_per_s"],
         "naive_per_page_memcpy_gbps": round(r["naive"]["gbps"], 3) if r.get("naive") else None}
     r = run_layerwise(sub, torch, kv, W)
     lw = r["layerwise"]
@@ -2077,10 +2087,12 @@ def run_single(args, torch, kv, W, k):
                    "io_stream": _IO.get("kind")},
         "tokens_per_s": round(2 * T / (step_ms * 1e-3), 1),
         "load": {"ms": round(load_ms, 4), "gbps": round(load_gbps, 3), "tokens_per_s": round(T / (load_ms * 1e-3), 1),
-                 "frac_of_h2d_peak": round(frac_h2d, 4) if peak else None},
+                 "frac_of_h2d_peak": round(frac_h2d, 4) if peak else None,
+                 "frac_of_kernel_h2d_peak": round(load_gbps / peak["kernel_h2d"], 4) if peak else None},
         "offload": {"ms": round(off_ms, 4), "gbps": round(off_gbps, 3),
                     "tokens_per_s": round(T / (off_ms * 1e-3), 1),
-                    "frac_of_d2h_peak": round(frac_d2h, 4) if peak else None},
+                    "frac_of_d2h_peak": round(frac_d2h, 4) if peak else None,
+                    "frac_of_kernel_d2h_peak": round(off_gbps / peak["kernel_d2h"], 4) if peak else None},
         "frac_of_host_link_peak": round(ideal_ms / step_ms, 4) if peak else None,
         "host_link_peak": peak_report(peak),
         "roofline": roofline(("kvio_head_major_kernel<load>" if args.host_layout == "head" else "kvio_copy_kernel<load>")

@@ -255,6 +255,18 @@ kvio_status kvio_naive_offload(kvio_pool_t pool, const kvio_span *spans, int32_t
  * the host-link peak that the transfers are measured against. */
 kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 
+/* One contiguous copy of `bytes` from src to dst by a plain kernel (16-byte
+ * vectors, 16 workgroups of 192 threads, enqueued on `stream`), in either
+ * direction between pinned host memory (kvio_host_alloc) and device memory,
+ * or within either.  It is the rate compute units reach on the host link with
+ * no paging at all: the ceiling of the kernel path, beside kvio_memcpy's
+ * copy-engine rate.  Defined by no passage of the paper; a measurement aid.
+ * bytes must be a multiple of 16 and both pointers 16-byte aligned
+ * (KVIO_EINVAL otherwise, before anything is enqueued); zero bytes is a
+ * no-op.  The caller owns both buffers and keeps them alive until the copy
+ * has completed on `stream`. */
+kvio_status kvio_kernel_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);
+
 /* Pinned, device-mapped host memory for host chunks (hipHostMalloc).
  * flags: KVIO_HOST_COHERENT (fine-grained, the default) or
  * KVIO_HOST_NONCOHERENT (coarse-grained).  The returned pointer is also the

@@ -10,7 +10,7 @@ from .kvio import (  # noqa: F401
     KVIO_HOST_COHERENT, KVIO_HOST_NONCOHERENT, KVIO_LAUNCH_CACHED, KVIO_MAX_SPANS_PER_LAUNCH,
     KVIO_HOST_TOKEN_MAJOR, KVIO_HOST_PAGE_FIRST, KVIO_HOST_HEAD_MAJOR, KVIO_LAUNCH_NO_LDS, KVIO_LAUNCH_STAGED,
     kvio_check, kvio_host_alloc, kvio_host_free, kvio_last_error, kvio_load, kvio_load_layer,
-    kvio_memcpy, kvio_naive_load, kvio_naive_offload, kvio_offload, kvio_pool_create,
+    kvio_memcpy, kvio_kernel_memcpy, kvio_naive_load, kvio_naive_offload, kvio_offload, kvio_pool_create,
     kvio_pool_destroy, kvio_span, kvio_strerror, launch, make_spans, Stream,
     kvio_stream_create, kvio_stream_destroy, kvio_schedule_round, kvio_disk_prefetch, kvio_disk_store_pages, DiskPrefetch,
     KVIO_DISK_PAGE_FIRST, KVIO_DISK_LAYER_FIRST, KVIO_EIO,

@@ -9,7 +9,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvio.so")
 SOURCES = [os.path.join(CSRC, "kvio_kernels.hip"), os.path.join(CSRC, "kvio_api.cpp"),
            os.path.join(CSRC, "kvio_sched.cpp"), os.path.join(CSRC, "kvio_disk.cpp"),
-           os.path.join(CSRC, "kvio_staged.cpp"), os.path.join(CSRC, "kvio_noalloc.hip")]
+           os.path.join(CSRC, "kvio_staged.cpp"), os.path.join(CSRC, "kvio_noalloc.hip"),
+           os.path.join(CSRC, "kvio_linkpeak.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

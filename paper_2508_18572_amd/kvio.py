@@ -113,6 +113,7 @@ def _load_library() -> ctypes.CDLL:
         "kvio_naive_load": [vp, ctypes.POINTER(kvio_span), i32, i32, i32, vp],
         "kvio_naive_offload": [vp, ctypes.POINTER(kvio_span), i32, i32, i32, vp],
         "kvio_memcpy": [vp, vp, ctypes.c_size_t, vp],
+        "kvio_kernel_memcpy": [vp, vp, ctypes.c_size_t, vp],
         "kvio_host_alloc": [ctypes.c_size_t, ctypes.c_uint32, ctypes.POINTER(vp)],
         "kvio_host_free": [vp],
         "kvio_stream_create": [ctypes.POINTER(ctypes.c_uint32), ctypes.c_uint32, ctypes.POINTER(vp)],
@@ -146,7 +147,7 @@ EXPORTS = ("kvio_pool_create", "kvio_pool_destroy", "kvio_load", "kvio_offload",
            "kvio_check", "kvio_naive_load", "kvio_naive_offload", "kvio_memcpy", "kvio_host_alloc",
            "kvio_host_free", "kvio_stream_create", "kvio_stream_destroy", "kvio_schedule_round",
            "kvio_disk_prefetch", "kvio_disk_store_pages", "kvio_disk_prefetch_start", "kvio_disk_prefetch_progress",
-           "kvio_disk_prefetch_finish", "kvio_load_noalloc",
+           "kvio_disk_prefetch_finish", "kvio_load_noalloc", "kvio_kernel_memcpy",
            "kvio_strerror", "kvio_last_error")
 
 
@@ -277,6 +278,10 @@ def kvio_naive_offload(pool: int, spans: Iterable[SpanLike], layer_begin: int, l
 
 def kvio_memcpy(dst: int, src: int, nbytes: int, stream=None) -> None:
     _check(_lib.kvio_memcpy(dst, src, nbytes, _stream(stream)))
+
+
+def kvio_kernel_memcpy(dst: int, src: int, nbytes: int, stream=None) -> None:
+    _check(_lib.kvio_kernel_memcpy(dst, src, nbytes, _stream(stream)))
 
 
 def kvio_host_alloc(nbytes: int, flags: int = KVIO_HOST_COHERENT) -> int:

@@ -73,6 +73,12 @@ def test_host_side_validation_without_device():
     assert e.value.status == kv.KVIO_EINVAL
     kv.kvio_pool_destroy(0)                                     # NULL is accepted
     kv.kvio_memcpy(0, 0, 0)                                     # zero bytes: no-op
+    kv.kvio_kernel_memcpy(0, 0, 0)
+    for dst, src, n, what in ((0, 4096, 16, "null"), (4096, 4096, 24, "multiple of 16"),
+                              (4104, 4096, 16, "aligned"), (4096, 4100, 32, "aligned")):
+        with pytest.raises(kv.KvioError) as e:                  # checked before anything is enqueued
+            kv.kvio_kernel_memcpy(dst, src, n)
+        assert e.value.status == kv.KVIO_EINVAL and what in e.value.detail
     lib = kv.kvio._lib                                          # stream arguments, checked before HIP
     out = ctypes.c_void_p()
     zero = (ctypes.c_uint32 * 2)()

@@ -814,3 +814,27 @@ def test_a_failed_runtime_call_does_not_leak_into_the_callers_next_call(kv):
         kv.kvio_host_alloc(1 << 52)                 # 4 PiB of pinned host memory
     assert e.value.status in (kv.KVIO_ENOMEM, kv.KVIO_EHIP)
     assert float(torch.ones(1 << 10, device="cuda").sum().item()) == float(1 << 10)
+
+
+@pytest.mark.parametrize("nbytes", [16, 1008, 16 * 1024 + 16, (5 << 20) + 48, (64 << 20) + 4096])
+def test_kernel_memcpy_both_directions(kv, nbytes):
+    """kvio_kernel_memcpy (the plain-kernel link ceiling) copies host -> device
+    and device -> host byte for byte, partial last steps and several grid
+    rounds included, and writes nothing past the end (sentinel tails)."""
+    import torch
+    src = kv.HostBuffer(nbytes)
+    src.array[:] = np.random.default_rng(nbytes).integers(0, 256, nbytes, dtype=np.uint8)
+    dev = torch.full((nbytes + 4096,), 0xA5, dtype=torch.uint8, device="cuda")
+    kv.kvio_kernel_memcpy(dev.data_ptr(), src.ptr, nbytes)
+    torch.cuda.synchronize()
+    got = dev.cpu().numpy()
+    assert np.array_equal(got[:nbytes], src.array)
+    assert (got[nbytes:] == 0xA5).all()
+    dst = kv.HostBuffer(nbytes + 4096)
+    dst.array[:] = 0x5A
+    kv.kvio_kernel_memcpy(dst.ptr, dev.data_ptr(), nbytes)
+    torch.cuda.synchronize()
+    assert np.array_equal(dst.array[:nbytes], src.array)
+    assert (dst.array[nbytes:] == 0x5A).all()
+    src.free()
+    dst.free()
