@@ -836,5 +836,10 @@ def test_kernel_memcpy_both_directions(kv, nbytes):
     torch.cuda.synchronize()
     assert np.array_equal(dst.array[:nbytes], src.array)
     assert (dst.array[nbytes:] == 0x5A).all()
+    dev2 = torch.full((nbytes + 4096,), 0x3C, dtype=torch.uint8, device="cuda")   # device -> device
+    kv.kvio_kernel_memcpy(dev2.data_ptr(), dev.data_ptr(), nbytes)
+    torch.cuda.synchronize()
+    assert torch.equal(dev2[:nbytes], dev[:nbytes])
+    assert bool((dev2[nbytes:] == 0x3C).all())
     src.free()
     dst.free()
