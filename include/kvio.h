@@ -262,8 +262,10 @@ kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t st
  * no paging at all: the ceiling of the kernel path, beside kvio_memcpy's
  * copy-engine rate.  Defined by no passage of the paper; a measurement aid.
  * bytes must be a multiple of 16 and both pointers 16-byte aligned
- * (KVIO_EINVAL otherwise, before anything is enqueued); zero bytes is a
- * no-op.  The caller owns both buffers and keeps them alive until the copy
+ * (KVIO_EINVAL otherwise), and each range must lie whole inside one
+ * allocation the device can reach (KVIO_ENOTMAPPED for memory the runtime
+ * does not know, KVIO_EINVAL for a range past its allocation's end); all
+ * checked before anything is enqueued.  Zero bytes is a no-op.  The caller owns both buffers and keeps them alive until the copy
  * has completed on `stream`. */
 kvio_status kvio_kernel_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 

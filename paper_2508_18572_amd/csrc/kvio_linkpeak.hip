@@ -58,8 +58,16 @@ extern "C" kvio_status kvio_kernel_memcpy(void *dst, const void *src, size_t byt
         return kvio::fail(KVIO_EINVAL, "%s: pointers must be 16-byte aligned", fn);
     if (bytes > static_cast<size_t>(INT64_MAX))
         return kvio::fail(KVIO_EINVAL, "%s: %zu bytes is too large", fn, bytes);
+    // Both ranges must lie in allocations the device can reach, whole: the
+    // kernel never touches memory past either.
+    const uint8_t *s = nullptr, *d = nullptr;
+    kvio_status st = kvio::device_view(src, bytes, false, "kvio_kernel_memcpy: source", &s);
+    if (st != KVIO_OK) return st;
+    st = kvio::device_view(dst, bytes, false, "kvio_kernel_memcpy: destination", &d);
+    if (st != KVIO_OK) return st;
     hipLaunchKernelGGL(kvio_plain_copy_kernel, dim3(kWorkgroups), dim3(kThreads), 0, stream,
-                       static_cast<const vec16 *>(src), static_cast<vec16 *>(dst), static_cast<int64_t>(bytes / 16));
+                       reinterpret_cast<const vec16 *>(s), reinterpret_cast<vec16 *>(const_cast<uint8_t *>(d)),
+                       static_cast<int64_t>(bytes / 16));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return kvio::fail_hip(e, fn);
     return KVIO_OK;

@@ -841,5 +841,12 @@ def test_kernel_memcpy_both_directions(kv, nbytes):
     torch.cuda.synchronize()
     assert torch.equal(dev2[:nbytes], dev[:nbytes])
     assert bool((dev2[nbytes:] == 0x3C).all())
+    with pytest.raises(kv.KvioError) as e:                      # past the end of the destination
+        kv.kvio_kernel_memcpy(dev2.data_ptr(), src.ptr, nbytes + 8192)
+    assert e.value.status == kv.KVIO_EINVAL and "allocation holds only" in e.value.detail
+    pageable = np.zeros(nbytes, np.uint8)                        # memory the runtime does not know
+    with pytest.raises(kv.KvioError) as e:
+        kv.kvio_kernel_memcpy(pageable.ctypes.data, dev.data_ptr(), nbytes)
+    assert e.value.status == kv.KVIO_ENOTMAPPED
     src.free()
     dst.free()
