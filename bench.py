@@ -899,7 +899,10 @@ def run_batched(args, torch, kv, W):
                              peak["h2d"] if peak else None, traffic=traffic,
                              algorithmic_bytes_per_launch=round(total / n_w),
                              algorithmic_traffic_per_launch=round(2 * total / n_w),
-                             launches_per_step=n_w),
+                             launches_per_step=n_w,
+                             plain_kernel_copy_peak=round(peak["kernel_h2d"], 3) if peak else None,
+                             frac_of_plain_kernel_copy_peak=round(load_gbps / peak["kernel_h2d"], 4)
+                             if peak else None),
         "cpu_baseline": cpu,
         "cpu_baseline_all_cores": cpu_all,
     })
