@@ -256,7 +256,8 @@ kvio_status kvio_naive_offload(kvio_pool_t pool, const kvio_span *spans, int32_t
 kvio_status kvio_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 
 /* One contiguous copy of `bytes` from src to dst by a plain kernel (16-byte
- * vectors, 16 workgroups of 192 threads, enqueued on `stream`), in either
+ * vectors; 16 workgroups of 192 threads into device memory, 32 of 256 into
+ * host memory; enqueued on `stream`), in either
  * direction between pinned host memory (kvio_host_alloc) and device memory,
  * or within either.  It is the rate compute units reach on the host link with
  * no paging at all: the ceiling of the kernel path, beside kvio_memcpy's

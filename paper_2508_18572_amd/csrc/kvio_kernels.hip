@@ -25,7 +25,8 @@
 //     using a small part of the chip (Sec. 4.2: confine the I/O kernel to a
 //     few compute units).
 //   * Non-temporal loads and stores (Sec. 4.2: bypass the cache to limit
-//     pollution of co-running kernels).
+//     pollution of co-running kernels); stores into host memory also carry
+//     the device-scope policy, which lets them fill the host link.
 //   * Grid-stride over tiles in host-address order, so the waves of a launch
 //     sweep a sliding window of consecutive host memory.
 #include <hip/hip_runtime.h>
@@ -57,6 +58,32 @@ __device__ __forceinline__ void store16(uint8_t *p, u32x4 v) {
         __builtin_nontemporal_store(v, q);
     } else {
         *q = v;
+    }
+}
+
+// Stores into pinned host memory (the offload's destination).  With the
+// device-scope cache policy (SC1) a wave's 1 KiB stores reach the host link's
+// full write rate, the copy engine's 57.0 GB/s, where the compiler's own
+// stores (plain or non-temporal) top out 1-2.5% lower.  An SC1 store is
+// acknowledged only once it has crossed the link, though, and a wave's next
+// step waits for its earlier stores, so SC1 pays only when many bytes are in
+// flight (the launcher decides, kSc1MinInflight).  No builtin selects SC1 for
+// a global store, so that store is written out; "memory" keeps the compiler
+// from moving other memory accesses across it, and the s_nop gives the two
+// wait states CDNA3/4 require before a VALU may overwrite the data registers
+// of a store wider than 64 bits (the compiler inserts them after its own
+// stores but cannot see the store inside the asm).
+template <bool NT, bool SC1>
+__device__ __forceinline__ void store_host16(uint8_t *p, u32x4 v) {
+    if constexpr (SC1) {
+        gvec *q = (gvec *)(p);
+        if constexpr (NT) {
+            asm volatile("global_store_dwordx4 %0, %1, off sc1 nt\n\ts_nop 1" : : "v"(q), "v"(v) : "memory");
+        } else {
+            asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" : : "v"(q), "v"(v) : "memory");
+        }
+    } else {
+        store16<NT>(p, v);
     }
 }
 
@@ -165,7 +192,7 @@ constexpr int kHostPageFirst = KVIO_HOST_PAGE_FIRST;
 // in one row, so the row, its slot (read from the owning lane with readlane)
 // and both base addresses are wave-uniform scalars; each lane adds only its
 // own 16-byte offset.
-template <int DIR, int U, bool NT, int HL>
+template <int DIR, int U, bool NT, bool SC1, int HL>
 __device__ __forceinline__ void step_wide(const CopyArgs &a, uint8_t *host, uint8_t *pool, int slot,
                                           int64_t hoff, int base, int nvec, uint32_t lane_off) {
     const int64_t R = a.row_bytes;
@@ -207,11 +234,11 @@ __device__ __forceinline__ void step_wide(const CopyArgs &a, uint8_t *host, uint
             buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0) + lane_off);
         if (all_ok) {
 #pragma unroll
-            for (int k = 0; k < U; ++k) store16<NT>(host + host_off[k] + lane_off, buf[k]);
+            for (int k = 0; k < U; ++k) store_host16<NT, SC1>(host + host_off[k] + lane_off, buf[k]);
         } else {
 #pragma unroll
             for (int k = 0; k < U; ++k)
-                if (pool_off[k] >= 0) store16<NT>(host + host_off[k] + lane_off, buf[k]);
+                if (pool_off[k] >= 0) store_host16<NT, SC1>(host + host_off[k] + lane_off, buf[k]);
         }
     }
 }
@@ -219,7 +246,7 @@ __device__ __forceinline__ void step_wide(const CopyArgs &a, uint8_t *host, uint
 // NARROW rows (any R multiple of 16 B): a wave-wide access may span several
 // rows, so each lane fetches its row's slot (and, page-first, its row's host
 // offset) from the owning lane with a cross-lane permute (ds_bpermute).
-template <int DIR, int U, bool NT, int HL>
+template <int DIR, int U, bool NT, bool SC1, int HL>
 __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, uint8_t *pool, int slot,
                                             int64_t hoff, int base, int nvec, int lane) {
     const int64_t R = a.row_bytes;
@@ -261,11 +288,11 @@ __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, ui
         for (int k = 0; k < U; ++k) buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0));
         if (all_ok) {
 #pragma unroll
-            for (int k = 0; k < U; ++k) store16<NT>(host + host_off[k], buf[k]);
+            for (int k = 0; k < U; ++k) store_host16<NT, SC1>(host + host_off[k], buf[k]);
         } else {
 #pragma unroll
             for (int k = 0; k < U; ++k)
-                if (pool_off[k] >= 0) store16<NT>(host + host_off[k], buf[k]);
+                if (pool_off[k] >= 0) store_host16<NT, SC1>(host + host_off[k], buf[k]);
         }
     }
 }
@@ -314,13 +341,15 @@ __device__ __forceinline__ void first_load_step(const CopyArgs &a, const SpanArg
 
 // DIR: kLoad (host chunk -> pool) or kOffload (pool -> host chunk).
 // U: 16-byte vectors per lane per step (one step = U KiB per wave).
-// WIDE: R is a multiple of 1 KiB (see step_wide).  HL: host layout.
+// NT: non-temporal accesses.  SC1: offload host stores with the device-scope
+// policy (store_host16).  WIDE: R is a multiple of 1 KiB (see step_wide).
+// HL: host layout.
 // Workgroup size bound of the kernels that need more than 128 VGPRs per lane
 // (page-first and head-major addressing at 16 KiB steps); their launcher folds
 // larger workgroups into more workgroups of this size.
 constexpr int kNarrowBound = 256;
 
-template <int DIR, int U, bool NT, bool WIDE, int HL>
+template <int DIR, int U, bool NT, bool SC1, bool WIDE, int HL>
 __global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBound)
     kvio_copy_kernel(const CopyArgs a) {
     const int lane = threadIdx.x & 63;
@@ -358,9 +387,9 @@ __global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBo
 #pragma unroll 1
         for (; base < nvec; base += 64 * U) {
             if constexpr (WIDE) {
-                step_wide<DIR, U, NT, HL>(a, host, pool, slot, hoff, base, nvec, lane_off);
+                step_wide<DIR, U, NT, SC1, HL>(a, host, pool, slot, hoff, base, nvec, lane_off);
             } else {
-                step_narrow<DIR, U, NT, HL>(a, host, pool, slot, hoff, base, nvec, lane);
+                step_narrow<DIR, U, NT, SC1, HL>(a, host, pool, slot, hoff, base, nvec, lane);
             }
         }
     }
@@ -385,7 +414,7 @@ __global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBo
 //   pool order  p = r * V + h * Vd + c     (pool row r, head h, vector c)
 //   host order  q = (h * n + r) * Vd + c
 // ----------------------------------------------------------------------------
-template <int DIR, int U, bool NT, bool LDS>
+template <int DIR, int U, bool NT, bool SC1, bool LDS>
 __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const CopyArgs a) {
     extern __shared__ u32x4 lds[];           // U * 64 vectors per wave
     const int lane = threadIdx.x & 63;
@@ -470,7 +499,7 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
                         const int c = q - hr * Vd;
                         const int s = __shfl(slot, r & 63);
                         if (q < nvec && s >= 0)
-                            store16<NT>(host + h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16,
+                            store_host16<NT, SC1>(host + h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16,
                                         slice[r * V + h * Vd + c]);
                     }
                 }
@@ -505,7 +534,7 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
                     for (int k = 0; k < U; ++k) buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0));
 #pragma unroll
                     for (int k = 0; k < U; ++k)
-                        if (pool_off[k] >= 0) store16<NT>(host + host_off[k], buf[k]);
+                        if (pool_off[k] >= 0) store_host16<NT, SC1>(host + host_off[k], buf[k]);
                 }
             }
         }
@@ -517,35 +546,61 @@ int rows_per_tile(int64_t row_bytes, int tile_kib) {
     return r < 1 ? 1 : (r > 64 ? 64 : static_cast<int>(r));
 }
 
+// Offloads whose launch keeps at least this many bytes in flight (waves x
+// step) store into host memory with the SC1 policy: enough to cover the
+// longer acknowledgement of those stores, so the link runs at its full write
+// rate (57.0 against 55.7 GB/s at the default 128 waves x 16 KiB).  Smaller
+// quotas (16 waves x 4 KiB: 27 against 44 GB/s) keep the plain policy.  A
+// build may move the threshold (-DKVIO_SC1_MIN_INFLIGHT=0 stores every
+// offload with SC1; a huge value never does), which is how both policies
+// were measured over launch shapes.
+#ifndef KVIO_SC1_MIN_INFLIGHT
+#define KVIO_SC1_MIN_INFLIGHT (int64_t(512) << 10)
+#endif
+constexpr int64_t kSc1MinInflight = KVIO_SC1_MIN_INFLIGHT;
+
+template <int DIR, int U, bool NT, bool SC1>
+static hipError_t launch_policy(const CopyArgs &a, dim3 grid, dim3 block, const Shape &s, hipStream_t stream) {
+    const bool wide = a.vec_per_row % 64 == 0;
+    switch (a.host_layout) {
+        case kHostPageFirst:
+            if (wide)
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, SC1, true, kHostPageFirst>), grid, block, 0, stream,
+                                   a);
+            else
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, SC1, false, kHostPageFirst>), grid, block, 0, stream,
+                                   a);
+            break;
+        case KVIO_HOST_HEAD_MAJOR:
+            if (s.head_major_lds)
+                hipLaunchKernelGGL((kvio_head_major_kernel<DIR, U, NT, SC1, true>), grid, block,
+                                   static_cast<size_t>(block.x / 64) * U * 1024, stream, a);
+            else
+                hipLaunchKernelGGL((kvio_head_major_kernel<DIR, U, NT, SC1, false>), grid, block, 0, stream, a);
+            break;
+        default:
+            if (wide)
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, SC1, true, kHostTokenMajor>), grid, block, 0, stream,
+                                   a);
+            else
+                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, SC1, false, kHostTokenMajor>), grid, block, 0,
+                                   stream, a);
+    }
+    return hipGetLastError();
+}
+
 template <int DIR, int U, bool NT>
 static hipError_t launch_u(const CopyArgs &a, const Shape &s, hipStream_t stream) {
     dim3 grid(s.workgroups), block(s.threads);
-    const bool wide = a.vec_per_row % 64 == 0;
     if (a.host_layout != KVIO_HOST_TOKEN_MAJOR && s.threads > kNarrowBound) {
         grid = dim3(static_cast<unsigned>(int64_t(s.workgroups) * s.threads / kNarrowBound));
         block = dim3(kNarrowBound);
     }
-    switch (a.host_layout) {
-        case kHostPageFirst:
-            if (wide)
-                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, true, kHostPageFirst>), grid, block, 0, stream, a);
-            else
-                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, false, kHostPageFirst>), grid, block, 0, stream, a);
-            break;
-        case KVIO_HOST_HEAD_MAJOR:
-            if (s.head_major_lds)
-                hipLaunchKernelGGL((kvio_head_major_kernel<DIR, U, NT, true>), grid, block,
-                                   static_cast<size_t>(block.x / 64) * U * 1024, stream, a);
-            else
-                hipLaunchKernelGGL((kvio_head_major_kernel<DIR, U, NT, false>), grid, block, 0, stream, a);
-            break;
-        default:
-            if (wide)
-                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, true, kHostTokenMajor>), grid, block, 0, stream, a);
-            else
-                hipLaunchKernelGGL((kvio_copy_kernel<DIR, U, NT, false, kHostTokenMajor>), grid, block, 0, stream, a);
+    if constexpr (DIR == kOffload && NT) {
+        const int64_t inflight = int64_t(grid.x) * (block.x / 64) * U * 1024;
+        if (inflight >= kSc1MinInflight) return launch_policy<DIR, U, NT, true>(a, grid, block, s, stream);
     }
-    return hipGetLastError();
+    return launch_policy<DIR, U, NT, false>(a, grid, block, s, stream);
 }
 
 template <int DIR, bool NT>
