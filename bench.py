@@ -98,6 +98,10 @@ def parse():
                     help="resource-quota sweep (Strata Fig. 5 analogue): load GB/s and the slowdown of a "
                          "co-running Llama-3.1-8B prefill pass (2 x 4K tokens) or decoding step (16 x 4K) vs. "
                          "the load's quota and CU placement, on the Llama-3.1-8B page-size-1 workload")
+    ap.add_argument("--quotas", type=str, default="",
+                    help="--interference: unmasked load quotas as WGxTHREADS,... (default: the full sweep)")
+    ap.add_argument("--masked", type=str, default="",
+                    help="--interference: CU partitions as NCUS:WGxTHREADS,... ('none' for no partition rows)")
     ap.add_argument("--page-sweep", action="store_true",
                     help="Llama-3.1-8B KV: kvio vs one hipMemcpyAsync per page segment over page sizes "
                          "1..256 (32K tokens), plus 8192 tokens at page size 32")
@@ -1204,7 +1208,10 @@ def run_interference(args, torch, kv, W):
 
     Residency rows: one idle wave (torch's one-thread spin kernel, no memory
     traffic) in place of the load, and the load with one one-wave workgroup
-    per CU (256 x 64), which leaves no CU without a resident wave."""
+    per CU (256 x 64), which leaves no CU without a resident wave.
+
+    --quotas and --masked replace the default unmasked quotas and CU
+    partitions with the ones listed."""
     k = 2
     wl = W.WORKLOADS[k]
     shp = wl.shape
@@ -1295,6 +1302,14 @@ def run_interference(args, torch, kv, W):
     rows = []
     quotas = [(1, 1024), (2, 1024), (4, 1024), (8, 256), (8, 512), (8, 1024), (16, 192), (16, 256), (32, 64),
               (64, 64), (256, 64)]
+    if args.quotas:
+        quotas = [tuple(int(x) for x in q.split("x")) for q in args.quotas.split(",")]
+    partitions = [(16, (16, 192)), (12, (12, 256)), (8, (8, 384)), (8, (8, 256)), (8, (8, 192)), (32, (32, 128))]
+    if args.masked == "none":
+        partitions = []
+    elif args.masked:
+        partitions = [(int(n), tuple(int(x) for x in q.split("x")))
+                      for n, q in (m.split(":") for m in args.masked.split(","))]
     for wg, th in quotas:
         pool = kv.KVPool(pool_t, P, load_launch=kv.launch(wg, th, 4, 0))
         row = {"placement": "unmasked", "workgroups": wg, "threads": th, "waves": wg * th // 64,
@@ -1332,8 +1347,7 @@ def run_interference(args, torch, kv, W):
     log("idle wave: " + ", ".join(f"{k2} {v}" for k2, v in row.items() if k2 != "placement"))
     # CU partitions: the load on a stream masked to the first n CUs (one workgroup
     # per CU; 24 to 64 waves), the co-runner on a stream masked to the rest.
-    for n_io, (wg, th) in ((16, (16, 192)), (12, (12, 256)), (8, (8, 384)), (8, (8, 256)), (8, (8, 192)),
-                           (32, (32, 128))):
+    for n_io, (wg, th) in partitions:
         try:
             io_m = kv.Stream(list(range(n_io)))
         except kv.KvioError as e:
