@@ -402,6 +402,8 @@ void common_args(const PoolGeom &g, uint8_t *const *layers, unsigned long long *
     a->page_shift = ilog2_exact(g.page_size);
     a->vec_per_row = static_cast<int32_t>(R / 16);
     a->vec_shift = ilog2_exact(R / 16);
+    a->vec_step_rows = static_cast<int32_t>(64 / (R / 16));
+    a->vec_step_cols = static_cast<int32_t>(64 % (R / 16));
     a->rows_per_tile = kvio::rows_per_tile(R, shape.tile_kib);
     a->host_layout = g.host_layout;
     a->num_heads = g.num_heads;

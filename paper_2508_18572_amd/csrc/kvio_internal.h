@@ -42,6 +42,8 @@ struct CopyArgs {
     int32_t page_shift;            // log2(P) when P is a power of two, else -1
     int32_t vec_per_row;           // V = R / 16
     int32_t vec_shift;             // log2(V) when V is a power of two, else -1
+    int32_t vec_step_rows;         // 64 / V: rows a lane's vector index advances per 64 vectors
+    int32_t vec_step_cols;         // 64 % V: and columns (carried into the row at V)
     int32_t rows_per_tile;         // 1 .. 64
     int32_t n_spans;               // spans in this launch, 1 .. KVIO_MAX_SPANS_PER_LAUNCH
     int32_t host_layout;           // KVIO_HOST_*

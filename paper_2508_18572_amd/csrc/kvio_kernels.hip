@@ -148,6 +148,27 @@ __device__ __forceinline__ int row_of(const CopyArgs &a, int v) {
     return a.vec_shift >= 0 ? (v >> a.vec_shift) : (v / a.vec_per_row);
 }
 
+// Row and column of one lane's vectors of a step, which lie 64 apart: from
+// vector j to j + 64 the row grows by 64 / V and the column by 64 % V (< V),
+// with at most one carry, so only the first vector needs a division.
+struct RowCol {
+    int r, c;
+};
+
+__device__ __forceinline__ RowCol rowcol_of(const CopyArgs &a, int j) {
+    const int r = row_of(a, j);
+    return {r, j - r * a.vec_per_row};
+}
+
+__device__ __forceinline__ void advance64(const CopyArgs &a, RowCol &p) {
+    p.r += a.vec_step_rows;
+    p.c += a.vec_step_cols;
+    if (p.c >= a.vec_per_row) {
+        p.c -= a.vec_per_row;
+        ++p.r;
+    }
+}
+
 // Lane r < nrows, page-first host chunk (the layers of one context page stored
 // together, Sec. 4.2.1 / Fig. 6): byte offset of row (layer, kv, t0 + r) from
 // the chunk start.  Rows of one page are contiguous; pages are L * 2 * P rows
@@ -246,53 +267,82 @@ __device__ __forceinline__ void step_wide(const CopyArgs &a, uint8_t *host, uint
 // NARROW rows (any R multiple of 16 B): a wave-wide access may span several
 // rows, so each lane fetches its row's slot (and, page-first, its row's host
 // offset) from the owning lane with a cross-lane permute (ds_bpermute).
+// Which vectors move is kept as a bit mask, and token-major host addresses
+// are formed where they are used, so at 16 KiB steps the kernel stays inside
+// the 128 registers a 1024-thread workgroup leaves each lane: only the U
+// loaded vectors and the U pool offsets of one direction are live at once.
 template <int DIR, int U, bool NT, bool SC1, int HL>
 __device__ __forceinline__ void step_narrow(const CopyArgs &a, uint8_t *host, uint8_t *pool, int slot,
                                             int64_t hoff, int base, int nvec, int lane) {
+    static_assert(U <= 32, "the move mask holds one bit per vector");
     const int64_t R = a.row_bytes;
-    const int V = a.vec_per_row;
-    int64_t pool_off[U];                    // this lane's vector k offset in the pool layer, -1 = skip
-    int64_t host_off[U];                    // and its offset from `host`
-    bool ok = true;
-#pragma unroll
-    for (int k = 0; k < U; ++k) {
-        const int j = base + k * 64 + lane;
-        const int r = row_of(a, j);
-        const int c = j - r * V;
-        const int s = __shfl(slot, r & 63);
-        pool_off[k] = (j < nvec && s >= 0) ? static_cast<int64_t>(s) * R + c * 16 : -1;
-        if constexpr (HL == kHostPageFirst)
-            host_off[k] = __shfl(static_cast<long long>(hoff), r & 63) + c * 16;
-        else
-            host_off[k] = static_cast<int64_t>(j) * 16;
-        ok = ok && pool_off[k] >= 0;
-    }
-    const bool all_ok = __all(ok);          // wave-uniform
-    u32x4 buf[U];
-    if (DIR == kLoad) {
+    const RowCol p0 = rowcol_of(a, base + lane);   // this lane's vector 0 of the step
+    int sl[U];                              // vector k: the slot of its row
+    int64_t host_off[HL == kHostPageFirst ? U : 1];   // page-first: its offset from `host`
+    uint32_t moves = 0;                     // bit k: vector k moves
+    auto resolve = [&]() {
+        RowCol p = p0;
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            const int j = base + k * 64 + lane;
-            buf[k] = load16<NT>(j < nvec ? host + host_off[k] : pool);
+            sl[k] = __shfl(slot, p.r & 63);
+            if constexpr (HL == kHostPageFirst)
+                host_off[k] = __shfl(static_cast<long long>(hoff), p.r & 63) + p.c * 16;
+            moves |= (base + k * 64 + lane < nvec && sl[k] >= 0) ? (1u << k) : 0u;
+            advance64(a, p);
         }
-        if (all_ok) {
+    };
+    // Byte offset in the pool layer of vector k at row/column p (0 for a
+    // vector that does not move: an in-bounds read, discarded).
+    auto pool_at = [&](int k, const RowCol &p) -> int64_t {
+        return ((moves >> k) & 1u) ? static_cast<int64_t>(sl[k]) * R + p.c * 16 : 0;
+    };
+    // This lane's vector k of a token-major chunk sits (base + k * 64 + lane) * 16
+    // bytes from `host`.
+    uint8_t *const host_lane = host + (static_cast<int64_t>(base) + lane) * 16;
+    auto host_at = [&](int k) -> uint8_t * {
+        if constexpr (HL == kHostPageFirst)
+            return host + host_off[k];
+        else
+            return host_lane + k * 1024;
+    };
+    constexpr uint32_t kAll = U == 32 ? ~0u : (1u << U) - 1u;
+    u32x4 buf[U];
+    RowCol p = p0;
+    if (DIR == kLoad) {
+        // Token-major host reads need no slot, so they go out first and the
+        // slots are resolved while they are in flight.
+        if constexpr (HL == kHostPageFirst) resolve();
 #pragma unroll
-            for (int k = 0; k < U; ++k) store16<NT>(pool + pool_off[k], buf[k]);
+        for (int k = 0; k < U; ++k)
+            buf[k] = load16<NT>(base + k * 64 + lane < nvec ? host_at(k) : pool);
+        if constexpr (HL != kHostPageFirst) resolve();
+        if (__all(moves == kAll)) {
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                store16<NT>(pool + pool_at(k, p), buf[k]);
+                advance64(a, p);
+            }
         } else {
 #pragma unroll
-            for (int k = 0; k < U; ++k)
-                if (pool_off[k] >= 0) store16<NT>(pool + pool_off[k], buf[k]);
+            for (int k = 0; k < U; ++k) {
+                if ((moves >> k) & 1u) store16<NT>(pool + pool_at(k, p), buf[k]);
+                advance64(a, p);
+            }
         }
     } else {
+        resolve();
 #pragma unroll
-        for (int k = 0; k < U; ++k) buf[k] = load16<NT>(pool + (pool_off[k] >= 0 ? pool_off[k] : 0));
-        if (all_ok) {
+        for (int k = 0; k < U; ++k) {
+            buf[k] = load16<NT>(pool + pool_at(k, p));
+            advance64(a, p);
+        }
+        if (__all(moves == kAll)) {
 #pragma unroll
-            for (int k = 0; k < U; ++k) store_host16<NT, SC1>(host + host_off[k], buf[k]);
+            for (int k = 0; k < U; ++k) store_host16<NT, SC1>(host_at(k), buf[k]);
         } else {
 #pragma unroll
             for (int k = 0; k < U; ++k)
-                if (pool_off[k] >= 0) store_host16<NT, SC1>(host + host_off[k], buf[k]);
+                if ((moves >> k) & 1u) store_host16<NT, SC1>(host_at(k), buf[k]);
         }
     }
 }
@@ -308,34 +358,41 @@ __device__ __forceinline__ void first_load_step(const CopyArgs &a, const SpanArg
                                                 uint8_t *host, uint8_t *&pool, int &slot, int64_t hoff,
                                                 int nvec, int lane) {
     const int64_t R = a.row_bytes;
-    const int V = a.vec_per_row;
     const uint32_t lane_off = static_cast<uint32_t>(lane) * 16u;
-    int row[U], col[U];
-    int64_t host_off[U];
+    // Chunk k is (WIDE) vector k * 64 and the 63 after it, all in one row, or
+    // this lane's vector k * 64 + lane.  Rows and columns are walked again for
+    // the stores rather than kept, so only the U loaded vectors stay live
+    // across the slot lookup.
+    const RowCol p0 = rowcol_of(a, WIDE ? 0 : lane);
     u32x4 buf[U];
+    {
+        RowCol p = p0;
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-        const int j = k * 64 + (WIDE ? 0 : lane);          // WIDE: chunk k's first vector (uniform)
-        row[k] = row_of(a, j);
-        col[k] = j - row[k] * V;
-        if constexpr (HL == kHostPageFirst)
-            host_off[k] = (WIDE ? readlane64(hoff, row[k] & 63) : static_cast<int64_t>(__shfl(
-                                                                       static_cast<long long>(hoff), row[k] & 63))) +
-                          col[k] * 16;
-        else
-            host_off[k] = static_cast<int64_t>(j) * 16;
-        const bool valid = WIDE ? (k * 64 < nvec) : (j < nvec);
-        buf[k] = load16<NT>(valid ? host + host_off[k] + (WIDE ? lane_off : 0u) : host);
+        for (int k = 0; k < U; ++k) {
+            const int j = k * 64 + (WIDE ? 0 : lane);
+            const bool valid = WIDE ? (k * 64 < nvec) : (j < nvec);
+            int64_t host_off;
+            if constexpr (HL == kHostPageFirst)
+                host_off = (WIDE ? readlane64(hoff, p.r & 63)
+                                 : static_cast<int64_t>(__shfl(static_cast<long long>(hoff), p.r & 63))) +
+                           p.c * 16;
+            else
+                host_off = static_cast<int64_t>(j) * 16;
+            buf[k] = load16<NT>(valid ? host + host_off + (WIDE ? lane_off : 0u) : host);
+            advance64(a, p);
+        }
     }
     pool = a.layers[loc.kv * a.num_layers + loc.layer];
     slot = lane_slot(a, sp, loc.t0, loc.nrows, lane);
+    RowCol p = p0;
 #pragma unroll
     for (int k = 0; k < U; ++k) {
         const int j = k * 64 + (WIDE ? 0 : lane);
         const bool valid = WIDE ? (k * 64 < nvec) : (j < nvec);
-        const int s = WIDE ? __builtin_amdgcn_readlane(slot, row[k] & 63) : __shfl(slot, row[k] & 63);
+        const int s = WIDE ? __builtin_amdgcn_readlane(slot, p.r & 63) : __shfl(slot, p.r & 63);
         if (valid && s >= 0)
-            store16<NT>(pool + static_cast<int64_t>(s) * R + col[k] * 16 + (WIDE ? lane_off : 0u), buf[k]);
+            store16<NT>(pool + static_cast<int64_t>(s) * R + p.c * 16 + (WIDE ? lane_off : 0u), buf[k]);
+        advance64(a, p);
     }
 }
 
@@ -344,13 +401,19 @@ __device__ __forceinline__ void first_load_step(const CopyArgs &a, const SpanArg
 // NT: non-temporal accesses.  SC1: offload host stores with the device-scope
 // policy (store_host16).  WIDE: R is a multiple of 1 KiB (see step_wide).
 // HL: host layout.
-// Workgroup size bound of the kernels that need more than 128 VGPRs per lane
-// (page-first and head-major addressing at 16 KiB steps); their launcher folds
+// Workgroup size bound of the kernels that need more than the 128 VGPRs per
+// lane a 1024-thread workgroup leaves (page-first and head-major addressing,
+// and loads of narrow token-major rows at 16 KiB steps); their launcher folds
 // larger workgroups into more workgroups of this size.
 constexpr int kNarrowBound = 256;
 
+template <int DIR, int U, bool WIDE, int HL>
+constexpr bool needs_narrow_bound() {
+    return HL != KVIO_HOST_TOKEN_MAJOR || (DIR == kLoad && U == 16 && !WIDE);
+}
+
 template <int DIR, int U, bool NT, bool SC1, bool WIDE, int HL>
-__global__ void __launch_bounds__(HL == KVIO_HOST_TOKEN_MAJOR ? 1024 : kNarrowBound)
+__global__ void __launch_bounds__((needs_narrow_bound<DIR, U, WIDE, HL>() ? kNarrowBound : 1024))
     kvio_copy_kernel(const CopyArgs a) {
     const int lane = threadIdx.x & 63;
     const int waves_per_wg = blockDim.x >> 6;
@@ -592,7 +655,11 @@ static hipError_t launch_policy(const CopyArgs &a, dim3 grid, dim3 block, const 
 template <int DIR, int U, bool NT>
 static hipError_t launch_u(const CopyArgs &a, const Shape &s, hipStream_t stream) {
     dim3 grid(s.workgroups), block(s.threads);
-    if (a.host_layout != KVIO_HOST_TOKEN_MAJOR && s.threads > kNarrowBound) {
+    const bool wide = a.vec_per_row % 64 == 0;
+    const bool narrow_bound = a.host_layout != KVIO_HOST_TOKEN_MAJOR ||
+                              (wide ? needs_narrow_bound<DIR, U, true, kHostTokenMajor>()
+                                    : needs_narrow_bound<DIR, U, false, kHostTokenMajor>());
+    if (narrow_bound && s.threads > kNarrowBound) {
         grid = dim3(static_cast<unsigned>(int64_t(s.workgroups) * s.threads / kNarrowBound));
         block = dim3(kNarrowBound);
     }
