@@ -134,6 +134,11 @@ def test_parity_launch_shapes(kv, wg, threads, tile, flags):
     run_case(kv, 2, 8, 128, 1, 3000, [(777, 800), (3, 3)], launch=launch, seed=wg)
     run_case(kv, 2, 4, 64, 16, 4096, [(1000, 1024)], launch=launch, seed=wg + 1)
     run_case(kv, 1, 1, 8, 3, 300, [(70, 80)], launch=launch, seed=wg + 2)
+    # Rows of 24 and 96 vectors (384 B and 1536 B, narrow): a lane's vectors 64
+    # apart advance by 2 rows + 16 columns and by 0 rows + 64 columns, so the
+    # column carries into the row on some vectors and not on others.
+    run_case(kv, 2, 3, 64, 5, 2000, [(403, 410), (64, 64)], launch=launch, seed=wg + 3)
+    run_case(kv, 2, 12, 64, 2, 1200, [(301, 301), (5, 9)], launch=launch, seed=wg + 4)
 
 
 def _staging(slot_pages, P, R):
