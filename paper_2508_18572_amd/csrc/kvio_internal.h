@@ -74,17 +74,29 @@ struct Shape {
 //   reads slow both directions.
 //   Smaller loads: 16 x 4 waves.  A 2 MiB context is 512 tiles of 4 KiB,
 //   which 64 waves share evenly (8 each) and finish ~1 us sooner than 48.
-//   Offload: 32 workgroups x 4 waves with 16 KiB steps (55.7 GB/s).
+//   Offload: 32 workgroups x 4 waves with 16 KiB steps (57.0 GB/s with the
+//   device-scope host stores).
+// Two host layouts differ on large transfers (Llama-3.1-8B KV, 4 GiB, page
+// sizes 1 and 16):
+//   Head-major loads take 8 KiB steps: 57.45 GB/s against 56.0-56.8 at 4 KiB
+//   (the per-head runs of a tile are twice as long); 2 MiB contexts keep
+//   4 KiB (51.1 against 48.6 GB/s).
+//   Page-first offloads take 64 x 4 waves with 8 KiB steps: 56.8-56.9 GB/s
+//   against 56.0-56.1 with 128 waves of 16 KiB (the same 2 MiB in flight).
 constexpr int kDefaultThreads = 256;
 constexpr Shape kDefaultLoad = {16, 192, 4, true, true};
+constexpr Shape kDefaultLoadHeadMajor = {16, 192, 8, true, true};
 constexpr Shape kDefaultLoadSmall = {16, kDefaultThreads, 4, true, true};
 constexpr int64_t kSmallLoadBytes = int64_t(32) << 20;
 constexpr Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
+constexpr Shape kDefaultOffloadPageFirst = {64, kDefaultThreads, 8, true, true};
 
-// The default shape of a call that moves `bytes` in direction `dir`.
-inline Shape default_shape(int dir, int64_t bytes) {
-    if (dir != 0) return kDefaultOffload;
-    return bytes < kSmallLoadBytes ? kDefaultLoadSmall : kDefaultLoad;
+// The default shape of a call that moves `bytes` in direction `dir` between
+// the pool and host chunks of layout `host_layout` (KVIO_HOST_*).
+inline Shape default_shape(int dir, int64_t bytes, int host_layout) {
+    if (dir != 0) return host_layout == KVIO_HOST_PAGE_FIRST ? kDefaultOffloadPageFirst : kDefaultOffload;
+    if (bytes < kSmallLoadBytes) return kDefaultLoadSmall;
+    return host_layout == KVIO_HOST_HEAD_MAJOR ? kDefaultLoadHeadMajor : kDefaultLoad;
 }
 // Staged transfers: the scatter / gather between the HBM staging buffer and
 // the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at
