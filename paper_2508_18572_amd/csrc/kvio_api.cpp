@@ -480,7 +480,7 @@ kvio_status run_copy(kvio_pool_t p, const kvio_span *spans, int32_t n, int32_t l
                               kvio::kernel_shape(p->g, lc, kvio::kDefaultStaged), fn);
         lc = kvio_launch{0, 0, 0, lc.flags & ~KVIO_LAUNCH_STAGED};   // small: the kernel path, default shape
     }
-    const kvio::Shape shape = kvio::kernel_shape(p->g, lc, kvio::default_shape(dir, bytes, p->g.host_layout));
+    const kvio::Shape shape = kvio::kernel_shape(p->g, lc, kvio::default_shape(dir, bytes, p->g.host_layout, p->g.num_heads));
     return kvio::launch_spans(p->g, p->d_layers, p->d_err, rs.data(), n, l0, l1, dir, shape, stream, fn);
 }
 

@@ -76,13 +76,17 @@ struct Shape {
 //   which 64 waves share evenly (8 each) and finish ~1 us sooner than 48.
 //   Offload: 32 workgroups x 4 waves with 16 KiB steps (57.0 GB/s with the
 //   device-scope host stores).
-// Two host layouts differ on large transfers (Llama-3.1-8B KV, 4 GiB, page
-// sizes 1 and 16):
-//   Head-major loads take 8 KiB steps: 57.45 GB/s against 56.0-56.8 at 4 KiB
-//   (the per-head runs of a tile are twice as long); 2 MiB contexts keep
-//   4 KiB (51.1 against 48.6 GB/s).
-//   Page-first offloads take 64 x 4 waves with 8 KiB steps: 56.8-56.9 GB/s
-//   against 56.0-56.1 with 128 waves of 16 KiB (the same 2 MiB in flight).
+// Two host layouts differ on large transfers (2-4 GiB at page sizes 1 and 16,
+// rows of 1-32 KV heads x 128 bf16 dims):
+//   Head-major loads with 8 or more KV heads take 8 KiB steps.  A wave step
+//   reads step / H bytes from each head's run, and at 4 KiB with 8 heads
+//   those 512-byte runs cost up to 15% (57.3 against 48.7-56.9 GB/s at
+//   8 KiB); with 16 and 32 heads the two steps are within 0.4%, with 1-4
+//   heads 4 KiB is 0.1-0.2 GB/s ahead.  2 MiB contexts keep 4 KiB (51.1
+//   against 48.6 GB/s with 4 heads).
+//   Page-first offloads take 64 x 4 waves with 8 KiB steps: 56.6-57.1 GB/s
+//   against 56.0-57.0 with 128 waves of 16 KiB (the same 2 MiB in flight),
+//   ahead at every row width.
 constexpr int kDefaultThreads = 256;
 constexpr Shape kDefaultLoad = {16, 192, 4, true, true};
 constexpr Shape kDefaultLoadHeadMajor = {16, 192, 8, true, true};
@@ -92,11 +96,12 @@ constexpr Shape kDefaultOffload = {32, kDefaultThreads, 16, true, true};
 constexpr Shape kDefaultOffloadPageFirst = {64, kDefaultThreads, 8, true, true};
 
 // The default shape of a call that moves `bytes` in direction `dir` between
-// the pool and host chunks of layout `host_layout` (KVIO_HOST_*).
-inline Shape default_shape(int dir, int64_t bytes, int host_layout) {
+// the pool (rows of `num_heads` KV heads) and host chunks of layout
+// `host_layout` (KVIO_HOST_*).
+inline Shape default_shape(int dir, int64_t bytes, int host_layout, int num_heads) {
     if (dir != 0) return host_layout == KVIO_HOST_PAGE_FIRST ? kDefaultOffloadPageFirst : kDefaultOffload;
     if (bytes < kSmallLoadBytes) return kDefaultLoadSmall;
-    return host_layout == KVIO_HOST_HEAD_MAJOR ? kDefaultLoadHeadMajor : kDefaultLoad;
+    return host_layout == KVIO_HOST_HEAD_MAJOR && num_heads >= 8 ? kDefaultLoadHeadMajor : kDefaultLoad;
 }
 // Staged transfers: the scatter / gather between the HBM staging buffer and
 // the pool is HBM-bound, so it takes the whole chip (4 GiB of 2 KiB rows at

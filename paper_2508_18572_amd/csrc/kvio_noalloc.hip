@@ -105,7 +105,7 @@ extern "C" kvio_status kvio_load_noalloc(const kvio_pool_desc *desc, const kvio_
     if (e != hipSuccess) return kvio::fail_hip(e, fn);
     const kvio::Shape shape = kvio::kernel_shape(
         g, desc->load_launch,
-        kvio::default_shape(kvio::kLoad, tokens * 2 * (layer_end - layer_begin) * g.row_bytes, g.host_layout));
+        kvio::default_shape(kvio::kLoad, tokens * 2 * (layer_end - layer_begin) * g.row_bytes, g.host_layout, g.num_heads));
     return kvio::launch_spans(g, init.table, init.err, rs, n_spans, layer_begin, layer_end, kvio::kLoad, shape,
                               stream, fn);
 }
