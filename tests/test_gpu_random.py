@@ -13,7 +13,7 @@ import workloads as W
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = {0: oracle.TOKEN_MAJOR, 1: oracle.PAGE_FIRST, 2: oracle.HEAD_MAJOR}
-N_CASES = 320
+N_CASES = 1000
 
 
 @pytest.fixture(scope="module")
