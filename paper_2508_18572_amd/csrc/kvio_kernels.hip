@@ -97,20 +97,57 @@ struct TileLoc {
     int nrows;
 };
 
-__device__ __forceinline__ TileLoc locate(const CopyArgs &a, int64_t g) {
-    TileLoc L;
-    const int64_t plane = g / a.plane_tiles;
-    const int64_t w = g - plane * a.plane_tiles;
-    int lo = 0, hi = a.n_spans - 1;          // largest s with tile_prefix[s] <= w
+// Largest span s with tile_prefix[s] <= w (binary search over the spans).
+__device__ __forceinline__ int span_of(const CopyArgs &a, int64_t w, int lo) {
+    int hi = a.n_spans - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
         if (a.tile_prefix[mid] <= w) lo = mid; else hi = mid - 1;
     }
-    L.span = lo;
-    L.layer = a.layer_begin + static_cast<int>(plane >> 1);
-    L.kv = static_cast<int>(plane & 1);
-    L.t0 = (w - a.tile_prefix[lo]) * a.rows_per_tile;
-    const int64_t left = a.spans[lo].num_tokens - L.t0;
+    return lo;
+}
+
+// A wave's position in the tile order: plane, tile inside the plane and the
+// span that holds it.  The wave's tiles lie `stride` (the number of waves)
+// apart, so the next one is found from the last without a 64-bit division
+// or a search in the common case (same plane, same span).
+struct TileCursor {
+    int64_t plane;
+    int64_t w;
+    int span;
+};
+
+__device__ __forceinline__ TileCursor cursor_at(const CopyArgs &a, int64_t g) {
+    TileCursor c;
+    c.plane = g / a.plane_tiles;
+    c.w = g - c.plane * a.plane_tiles;
+    c.span = span_of(a, c.w, 0);
+    return c;
+}
+
+__device__ __forceinline__ void cursor_advance(const CopyArgs &a, TileCursor &c, int64_t stride) {
+    c.w += stride;
+    if (c.w >= a.plane_tiles) {                 // into a later plane: its spans start over
+        if (c.w < 2 * a.plane_tiles) {
+            c.w -= a.plane_tiles;
+            ++c.plane;
+        } else {
+            c.plane += c.w / a.plane_tiles;
+            c.w %= a.plane_tiles;
+        }
+        c.span = span_of(a, c.w, 0);
+    } else if (c.span + 1 < a.n_spans && a.tile_prefix[c.span + 1] <= c.w) {
+        c.span = span_of(a, c.w, c.span + 1);  // further on in the same plane
+    }
+}
+
+__device__ __forceinline__ TileLoc locate(const CopyArgs &a, const TileCursor &c) {
+    TileLoc L;
+    L.span = c.span;
+    L.layer = a.layer_begin + static_cast<int>(c.plane >> 1);
+    L.kv = static_cast<int>(c.plane & 1);
+    L.t0 = (c.w - a.tile_prefix[c.span]) * a.rows_per_tile;
+    const int64_t left = a.spans[c.span].num_tokens - L.t0;
     L.nrows = left < a.rows_per_tile ? static_cast<int>(left) : a.rows_per_tile;
     return L;
 }
@@ -423,9 +460,10 @@ __global__ void __launch_bounds__((needs_narrow_bound<DIR, U, WIDE, HL>() ? kNar
 
     int64_t g = static_cast<int64_t>(blockIdx.x) * waves_per_wg + wave_in_wg;
     bool first = DIR == kLoad;
+    TileCursor cur = cursor_at(a, g);
 #pragma unroll 1
-    for (; g < a.total_tiles; g += nwaves) {
-        const TileLoc loc = locate(a, g);
+    for (; g < a.total_tiles; g += nwaves, cursor_advance(a, cur, nwaves)) {
+        const TileLoc loc = locate(a, cur);
         const SpanArg &sp = a.spans[loc.span];
         uint8_t *host = const_cast<uint8_t *>(sp.host);
         int64_t hoff = 0;
@@ -490,10 +528,11 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
     const int Vd = a.seg_vecs;
     const int64_t De = static_cast<int64_t>(Vd) * 16;
 
+    int64_t g0 = static_cast<int64_t>(blockIdx.x) * waves_per_wg + wave_in_wg;
+    TileCursor cur = cursor_at(a, g0);
 #pragma unroll 1
-    for (int64_t g = static_cast<int64_t>(blockIdx.x) * waves_per_wg + wave_in_wg;
-         g < a.total_tiles; g += nwaves) {
-        const TileLoc loc = locate(a, g);
+    for (int64_t g = g0; g < a.total_tiles; g += nwaves, cursor_advance(a, cur, nwaves)) {
+        const TileLoc loc = locate(a, cur);
         const SpanArg &sp = a.spans[loc.span];
         uint8_t *pool = a.layers[loc.kv * a.num_layers + loc.layer];
         const int n = loc.nrows;
