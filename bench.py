@@ -86,6 +86,9 @@ def parse():
     ap.add_argument("--staged", action="store_true",
                     help="copy engine through an HBM staging buffer + scatter/gather kernel (KVIO_LAUNCH_STAGED)")
     ap.add_argument("--staging-mib", type=int, default=0, help="staging per direction (4 slots); 0 = default")
+    ap.add_argument("--cu-partition", type=int, default=0,
+                    help="--config 3: load on a stream masked to the first N CUs, GEMMs on a stream masked to "
+                         "the rest (0 = both streams over every CU)")
     ap.add_argument("--gemm-m", type=int, default=4096,
                     help="layer-wise workload: rows of the per-layer GEMM (4096 = load-bound; 65536 = compute-bound)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -612,6 +615,13 @@ def run_layerwise(args, torch, kv, W):
                      staging_bytes=args.staging_mib << 20)
     span = [(host.ptr, T, T, pidx.data_ptr())]
     side, comp = io_stream(torch, kv), torch.cuda.Stream()
+    masked = []
+    if args.cu_partition:
+        # The load on its own CUs, the GEMMs on the others: neither waits for
+        # CUs the other holds (Sec. 4.2: confine the I/O kernel to few CUs).
+        n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+        masked = [kv.Stream(list(range(args.cu_partition))), kv.Stream(list(range(args.cu_partition, n_cu)))]
+        side, comp = masked[0].torch, masked[1].torch
     M, N, K = args.gemm_m, 8192, 8192
     g = torch.Generator(device="cuda").manual_seed(W.data_seed(k))
     A = torch.randn(M, K, device="cuda", dtype=torch.bfloat16, generator=g)
@@ -639,13 +649,18 @@ def run_layerwise(args, torch, kv, W):
         return t.ms()[0]
 
     def both():
+        # Event handles exist before the timed region (torch creates one at its
+        # first record), so the side stream carries only the library's record.
+        evs_all = [torch.cuda.Event(enable_timing=True) for _ in range(L)]
+        for ev in evs_all:
+            ev.record(comp)
+        torch.cuda.synchronize()
         start = torch.cuda.Event(enable_timing=True)
         start.record(comp)
         side.wait_event(start)
         g0, g1, evs = [], [], []
         for l in range(L):
-            ev = torch.cuda.Event(enable_timing=True)
-            ev.record(side)                              # materialise the handle
+            ev = evs_all[l]
             pool.load_layer(span, l, stream=side, done=ev)
             evs.append(ev)
             comp.wait_event(ev)
@@ -686,7 +701,9 @@ def run_layerwise(args, torch, kv, W):
                       {"kv_shape": shp.name, "layers": L, "page_size": P, "pool_slots": S, "tokens": T,
                        "payload_bytes": nbytes, "bytes_per_layer_launch": per_layer,
                        "gemm_per_layer": [M, N, K], "step": "80 x (kvio_load_layer on a side stream; "
-                       "event; bf16 GEMM on the compute stream)"})
+                       "event; bf16 GEMM on the compute stream)",
+                       "cu_partition": (f"load on CUs 0-{args.cu_partition - 1}, GEMMs on the others"
+                                        if args.cu_partition else "none: both streams over every CU")})
     res.update({
         "tokens_per_s": round(T / (tl_co * 1e-3), 1),
         "layerwise": {"t_load_alone_ms": round(tl, 3), "t_gemm_alone_ms": round(tg, 3), "t_both_ms": round(tb, 3),
@@ -701,6 +718,8 @@ def run_layerwise(args, torch, kv, W):
         "reps": reps,
     })
     pool.close()
+    for st in masked:
+        st.close()
     del pool_t
     host.free()
     torch.cuda.empty_cache()
