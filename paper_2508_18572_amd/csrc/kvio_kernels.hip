@@ -152,10 +152,21 @@ __device__ __forceinline__ TileLoc locate(const CopyArgs &a, const TileCursor &c
     return L;
 }
 
-// Lane r < nrows: pool slot of token t0 + r, or -1 for rows past the tile or
-// an out-of-range page (recorded once in the error word, never dereferenced).
-__device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp,
-                                         int64_t t0, int nrows, int lane) {
+// Lane r < nrows: the pool page that the span's page table gives token t0 + r
+// (read only; checked by page_slot), or -1 for rows past the tile.
+__device__ __forceinline__ int32_t lane_page(const CopyArgs &a, const SpanArg &sp, int64_t t0, int nrows,
+                                             int lane) {
+    if (lane >= nrows) return -1;
+    const int64_t t = t0 + lane;
+    const int64_t cpage = a.page_shift >= 0 ? (t >> a.page_shift) : t / a.page_size;   // wave-uniform branch
+    return sp.page_idx[cpage];
+}
+
+// Lane r < nrows: pool slot of token t0 + r given its page from lane_page, or
+// -1 for rows past the tile or an out-of-range page (recorded once in the
+// error word, never dereferenced).
+__device__ __forceinline__ int page_slot(const CopyArgs &a, const SpanArg &sp, int64_t t0, int nrows, int lane,
+                                         int32_t page) {
     int slot = -1;
     if (lane < nrows) {
         const int64_t t = t0 + lane;
@@ -167,7 +178,6 @@ __device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp,
             cpage = t / a.page_size;
             off = t - cpage * a.page_size;
         }
-        const int32_t page = sp.page_idx[cpage];
         if (page >= 0 && page < a.num_pages) {
             slot = static_cast<int>(static_cast<int64_t>(page) * a.page_size + off);
         } else {
@@ -178,6 +188,11 @@ __device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp,
         }
     }
     return slot;
+}
+
+// Lane r < nrows: pool slot of token t0 + r (lane_page, then page_slot).
+__device__ __forceinline__ int lane_slot(const CopyArgs &a, const SpanArg &sp, int64_t t0, int nrows, int lane) {
+    return page_slot(a, sp, t0, nrows, lane, lane_page(a, sp, t0, nrows, lane));
 }
 
 // Row of vector v of a tile (v / V).
@@ -540,7 +555,17 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
         uint8_t *host = const_cast<uint8_t *>(sp.host) +
                         ((static_cast<int64_t>(loc.layer) * 2 + loc.kv) * a.num_heads * sp.host_tokens + loc.t0) * De;
         const int64_t head_stride = sp.host_tokens * De;
-        const int slot = lane_slot(a, sp, loc.t0, n, lane);
+        // The page-table read goes out first.  A load through LDS with steps of
+        // 8 KiB or more then issues its host reads and checks the page once
+        // they are in flight: the table read is older than them, so waiting
+        // for it leaves them outstanding (workload-size head-major loads:
+        // 57.2-57.3 against 56.8-56.9 GB/s).  With 4 KiB steps, the small-call
+        // default, checking first is faster (2 MiB contexts: 51.0 against
+        // 48.8-49.2 GB/s), and the other paths need the slot before their
+        // first access.
+        constexpr bool kLateSlot = LDS && DIR == kLoad && U >= 8;
+        const int32_t page = lane_page(a, sp, loc.t0, n, lane);
+        int slot = kLateSlot ? -1 : page_slot(a, sp, loc.t0, n, lane, page);
         const int nvec = n * V;
 #pragma unroll 1
         for (int base = 0; base < nvec; base += 64 * U) {
@@ -560,6 +585,7 @@ __global__ void __launch_bounds__(kNarrowBound) kvio_head_major_kernel(const Cop
                         buf[k] = load16<NT>(q < nvec ? host + h * head_stride + (static_cast<int64_t>(r) * Vd + c) * 16
                                                      : pool);
                     }
+                    slot = page_slot(a, sp, loc.t0, n, lane, page);
                     // All U loads are in flight before the first LDS write waits for one.
 #pragma unroll
                     for (int k = 0; k < U; ++k)
