@@ -383,6 +383,59 @@ def test_out_of_range_page_is_skipped_and_reported(kv):
         pool.close()
 
 
+@pytest.mark.parametrize("layout", [oracle.TOKEN_MAJOR, oracle.PAGE_FIRST, oracle.HEAD_MAJOR])
+@pytest.mark.parametrize("tile", [4, 8, 16])
+def test_out_of_range_page_every_layout_and_step(kv, layout, tile):
+    """The range check on every host layout and step size, both directions
+    (head-major loads with steps of 8 KiB or more check the page after their
+    host reads are issued).  Expected images come from the oracle run on a
+    pool one page larger, where the bad index is a valid page: its first S
+    slots are the GPU pool after the load, and the offload leaves untouched
+    exactly the host bytes that page would supply (found by running the
+    oracle with that page all zeros and all ones)."""
+    import torch
+    L, H, D, P, S, T = 2, 8, 128, 16, 1024, 64
+    R = H * D * 2
+    pool_np, pool_t = _pool(L, S, H, D, 60 + tile + 7 * layout)
+    pages = np.array([3, S // P, 7, 1], np.int32)         # context page 1 is out of range
+    pt = torch.from_numpy(pages).cuda()
+    nbytes = oracle.host_chunk_bytes(layout, L, T, R, P)
+    shape = kv.launch(0, 0, tile, 0)
+    with kv.HostBuffer(nbytes) as hb, kv.HostBuffer(nbytes) as ob:
+        W.fill_np(hb.array, 60 + tile, W.LLAMA8B)
+        ob.array[:] = 0x5A
+        pool = kv.KVPool(pool_t, P, load_launch=shape, offload_launch=shape, host_layout=layout)
+        try:
+            pool.load([(hb.ptr, T, T, pt.data_ptr())])
+            torch.cuda.synchronize()
+            with pytest.raises(kv.KvioError) as e:
+                pool.check()
+            assert e.value.status == kv.KVIO_ERANGE and "context page 1" in e.value.detail
+            big = np.zeros((2, L, S + P, R), np.uint8)
+            big[:, :, :S] = pool_np
+            oracle.load_layout(big[0], big[1], P, [(hb.array, T, T, pages)], layout, num_heads=H)
+            assert np.array_equal(_pool_bytes(pool_t), big[:, :, :S])
+            pool.offload([(ob.ptr, T, T, pt.data_ptr())])
+            torch.cuda.synchronize()
+            with pytest.raises(kv.KvioError) as e:
+                pool.check()
+            assert e.value.status == kv.KVIO_ERANGE and "context page 1" in e.value.detail
+            outs = []
+            for extra in (0x00, 0xFF):
+                b2 = big.copy()
+                b2[:, :, S:] = extra
+                eo = np.full(nbytes, 0x5A, np.uint8)
+                oracle.offload_layout(b2[0], b2[1], P, [(eo, T, T, pages)], layout, num_heads=H)
+                outs.append(eo)
+            exp = outs[0].copy()
+            skipped = outs[0] != outs[1]
+            assert skipped.sum() == L * 2 * P * R            # exactly that page's rows
+            exp[skipped] = 0x5A
+            assert np.array_equal(ob.array, exp)
+        finally:
+            pool.close()
+
+
 def test_validation_errors(kv):
     """Synchronous validation: nothing is enqueued, the pool is untouched."""
     import torch
