@@ -87,8 +87,9 @@ __device__ __forceinline__ void store_host16(uint8_t *p, u32x4 v) {
     }
 }
 
-// Locate global tile g: its plane (layer, K|V), span and first token.  All
-// operands are wave-uniform, so this runs on the scalar unit.
+// Where a tile lies: its span, plane (layer, K|V), first token and row count.
+// All of it is wave-uniform, so it is computed on the scalar unit (locate,
+// from the wave's TileCursor below).
 struct TileLoc {
     int span;
     int layer;
