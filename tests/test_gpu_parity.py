@@ -141,6 +141,22 @@ def test_parity_launch_shapes(kv, wg, threads, tile, flags):
     run_case(kv, 2, 12, 64, 2, 1200, [(301, 301), (5, 9)], launch=launch, seed=wg + 4)
 
 
+@pytest.mark.parametrize("wg,threads,why", [
+    (1, 256, "4 waves: the next tile is in the same plane"),
+    (2, 1024, "32 waves: the next tile is in the next plane (wrap)"),
+    (4, 1024, "64 waves: the next tile is planes further on (division)"),
+    (16, 64, "16 waves over many small spans: the span search"),
+])
+def test_tile_cursor_paths(kv, wg, threads, why):
+    """Each way a wave's tile cursor moves to its next tile, with planes of
+    20 tiles (40 tokens of 2 KiB rows in 4 KiB steps) over 12 planes, and a
+    run of one- to three-tile spans for the span search."""
+    launch = kv.launch(wg, threads, 4, 0)
+    run_case(kv, 6, 8, 128, 16, 2048, [(40, 40)], launch=launch, seed=wg)
+    run_case(kv, 6, 8, 128, 16, 4096, [(2 * (i % 3) + 1, 6) for i in range(30)] + [(0, 4), (5, 5)],
+             launch=launch, seed=wg + 50)
+
+
 def _staging(slot_pages, P, R):
     """staging_bytes whose 4 slots hold slot_pages pages of K and V rows each
     (0 = the library default), plus a few bytes the library rounds away."""
